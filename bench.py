@@ -1,0 +1,182 @@
+"""Throughput of the fused turn-KL forward + backward on one MI355X.
+
+Workload: the long-horizon agent batch, 65,536 packed tokens x vocabulary
+151,936 (bf16 logits), 30 trajectories with 20-50 turns of lognormal length,
+40% observation-masked, teacher noise decaying with turn depth, alpha = 0.5
+(synth/configs.py).  One step = one turnkl_fwd_bwd call: segments, weights,
+per-token reverse KL, the student-logit gradient for every row, the loss and
+the per-turn statistics.  Inputs are generated in HBM before timing.
+
+Prints one JSON line: tokens/s for the whole step, plus the row kernel's
+roofline (algorithmic bytes / measured duration against 8 TB/s) and the CPU
+oracle's throughput on a bounded sample of the same batch.
+"""
+import argparse
+import hashlib
+import json
+import os
+import re
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+HBM_PEAK_GBS = 8000.0
+ROW_KERNEL_SOURCES = ["paper_2607_05804_amd/csrc/rowkl.hip",
+                      "paper_2607_05804_amd/csrc/turnkl_internal.h",
+                      "paper_2607_05804_amd/csrc/block_ops.h"]
+COUNTER_FILE = os.path.join(ROOT, "profiles", "rowkl_long_horizon_counters.md")
+
+
+def row_kernel_digest() -> str:
+    h = hashlib.sha256()
+    for p in ROW_KERNEL_SOURCES:
+        with open(os.path.join(ROOT, p), "rb") as f:
+            h.update(f.read())
+    return h.hexdigest()[:16]
+
+
+def committed_traffic():
+    """HBM bytes per row-kernel launch from the committed counter summary,
+    or None when it is missing or was taken on a different kernel source."""
+    if not os.path.exists(COUNTER_FILE):
+        return None
+    txt = open(COUNTER_FILE).read()
+    m = re.search(r"kernel_source_digest:\s*([0-9a-f]+)", txt)
+    t = re.search(r"hbm_bytes_per_launch:\s*([0-9.eE+]+)", txt)
+    if not m or not t or m.group(1) != row_kernel_digest():
+        return None
+    return float(t.group(1))
+
+
+def cpu_baseline(w, sample_tokens: int):
+    """The float64 oracle, timed on a prefix of the batch (all its rows,
+    loss, gradient of every supervised row and per-turn stats)."""
+    import numpy as np
+    from oracle import turnkl_oracle as O
+
+    n = min(sample_tokens, w.n_tokens)
+    traj, turn, mask = w.traj_id[:n], w.turn_id[:n], w.loss_mask[:n]
+    sup = np.nonzero(mask)[0]
+    zs, zt = w.host_rows(np.arange(n))  # generated before the clock starts
+    src = lambda rows: (zs[rows], zt[rows])
+    t0 = time.perf_counter()
+    ref = O.fwd_bwd(traj, turn, mask, w.alphas[0], w.max_turns, src, O.DTYPE_BF16, 1.0,
+                    grad_rows=sup)
+    dt = time.perf_counter() - t0
+    assert ref.status == O.OK
+    return {"value": n / dt, "unit": "tokens/s", "cores": O.max_threads(), "kind": "oracle",
+            "sample": f"first {n} tokens of the batch ({sup.size} supervised rows, full "
+                      f"vocabulary {w.vocab}), {dt:.1f} s"}
+
+
+def main() -> int:
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--cpu-sample-tokens", type=int, default=4096)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print(f"bench.py runs on one GPU only (asked for --gpus {args.gpus}); the multi-GPU "
+              "layout is data-parallel by trajectory and is not built here.", file=sys.stderr)
+        return 2
+
+    import numpy as np
+    import torch
+
+    import synth
+    from paper_2607_05804_amd import turnkl as T
+
+    T.lib()  # fails loudly when the HIP library is missing
+    dev = torch.device("cuda:0")
+    w = synth.make("long_horizon")
+    alpha = w.alphas[0]
+    n, V = w.n_tokens, w.vocab
+    n_sup = w.n_supervised
+    zs, zt = w.device_logits(device=dev)
+    turn = torch.from_numpy(w.turn_id).to(dev)
+    traj = torch.from_numpy(w.traj_id).to(dev)
+    mask = torch.from_numpy(w.loss_mask).to(dev)
+    grad = torch.empty_like(zs)
+    stats = T.new_turn_stats(w.max_turns, device=dev)
+    kl = torch.empty(n, dtype=torch.float32, device=dev)
+    ws = T.Workspace(n, V, T.BF16, w.max_turns, device=dev)
+
+    def step():
+        return T.fwd_bwd(zs, zt, turn, traj, mask, alpha, grad=grad, max_turns=w.max_turns,
+                         turn_stats=stats, token_kl=kl, workspace=ws, check=False)
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    if ws.status() != T.OK:
+        raise RuntimeError(T.status_string(ws.status()))
+
+    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+          for _ in range(args.steps)]
+    for a, b in ev:  # materialise the events before the timed region
+        a.record()
+        b.record()
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for a, b in ev:
+        T.profile_row_kernel(a, b)
+        step()
+    T.profile_row_kernel(None, None)
+    torch.cuda.synchronize()
+    elapsed = time.perf_counter() - t0
+    if ws.status() != T.OK:
+        raise RuntimeError(T.status_string(ws.status()))
+
+    row_ms = float(np.mean([a.elapsed_time(b) for a, b in ev]))
+    ms_per_step = elapsed * 1e3 / args.steps
+    es = 2
+    row_bytes = n_sup * 3 * V * es + (n - n_sup) * V * es
+    achieved = row_bytes / (row_ms * 1e-3) / 1e9
+    traffic = committed_traffic()
+    out = {
+        "metric": "fused turn-KL fwd+bwd tokens/sec and achieved HBM GB/s (% of peak), V=151936",
+        "value": n * args.steps / elapsed,
+        "unit": "tokens/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": ms_per_step,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "f32",
+        "data": "synthetic",
+        "config": {
+            "workload": f"long-horizon agent batch: {n} tokens x V={V} bf16 logits, "
+                        f"{int(w.traj_id.max()) + 1} trajectories, 40% observation-masked, "
+                        f"alpha={alpha}",
+            "n_tokens": n, "vocab": V, "supervised_tokens": n_sup, "logits": "bf16",
+            "gradient": "bf16, out of place", "parallelism": "single GPU",
+        },
+        "roofline": {
+            "bound": "hbm",
+            "achieved": achieved,
+            "peak": HBM_PEAK_GBS,
+            "unit": "GB/s",
+            "frac": achieved / HBM_PEAK_GBS,
+            "traffic": traffic,
+            "kernel": "rowkl_kernel",
+            "kernel_ms": row_ms,
+            "algorithmic_bytes_per_launch": row_bytes,
+        },
+        "step_hbm_gbs": row_bytes / (ms_per_step * 1e-3) / 1e9,
+    }
+    del zs, zt, grad
+    torch.cuda.empty_cache()
+    if not args.no_cpu_baseline:
+        out["cpu_baseline"] = cpu_baseline(w, args.cpu_sample_tokens)
+    print(json.dumps(out), flush=True)
+    return 0
+
+
+if __name__ == "__main__":
+    sys.exit(main())

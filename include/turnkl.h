@@ -1,0 +1,203 @@
+/*
+ * turnkl.h -- fused turn-aware reverse-KL distillation loss for MI355X (gfx950).
+ *
+ * This is the data-parallel hot path of one TurnOPD training step (arXiv
+ * 2607.05804).  For a packed batch of multi-turn agent trajectories it
+ * computes, in one stream-ordered call:
+ *
+ *   1. the (trajectory, turn) segments of the batch and their supervised-token
+ *      counts (Sec. 3: a trace is x, o_1, r_1, ..., o_T, r_T and only response
+ *      tokens carry the loss mask; Sec. 4.4: n_t supervised tokens at turn t,
+ *      N = sum_t n_t);
+ *   2. the progressive turn-normalised token weights (Sec. 5.2:
+ *      q_traj_t = n_t / sum_j n_j, q_turn_t = 1 / T,
+ *      q_blend_t = (1 - alpha) q_traj_t + alpha q_turn_t; App. D, Algorithm 1:
+ *      w_blend = (1 - alpha) w_traj + alpha w_turn), averaged over
+ *      trajectories as the seq-mean-token-mean base aggregation does;
+ *   3. the per-token reverse KL D_KL(p_student || p_teacher) over the full
+ *      vocabulary (Sec. 3, Eq. opd-rkl; temperature 1, App. D);
+ *   4. its gradient with respect to the student logits (the teacher is
+ *      frozen, Sec. 3): G[i, v] = grad_scale * w_i * p_s(v) * (log p_s(v) -
+ *      log p_t(v) - KL_i);
+ *   5. the loss L = sum_i w_i KL_i (App. D, Algorithm 1), together with its
+ *      alpha = 0 and alpha = 1 forms;
+ *   6. per-turn-index statistics of the per-token KL (Sec. 4.3, Eq.
+ *      observed-turn-kl: K_t; Sec. 5.1 and App. D: survivors n_t and K_t feed
+ *      the rollout-depth controller; Sec. 4.4: s_t, the turn's loss share).
+ *
+ * Conventions for every entry point:
+ *   - Pointers are DEVICE pointers owned by the caller unless marked "host".
+ *     The library allocates no memory and keeps no per-call state; all
+ *     scratch lives in the caller's workspace.
+ *   - Work is enqueued on `stream` and is asynchronous; the success path never
+ *     synchronises with the host.  Calls on distinct workspaces may run
+ *     concurrently; calls sharing a workspace must be stream-ordered.
+ *   - Argument errors detectable on the host are returned synchronously before
+ *     anything is enqueued and leave every output untouched.
+ *   - Data-dependent errors (bad ids or mask) are detected on the device and
+ *     recorded in the workspace; turnkl_get_status returns them.
+ */
+#ifndef TURNKL_H_
+#define TURNKL_H_
+
+#include <stddef.h>
+#include <stdint.h>
+
+#include <hip/hip_runtime_api.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+/* Element type of the logits and of the gradient. */
+typedef enum {
+  TURNKL_BF16 = 0, /* bfloat16; the gradient is rounded to nearest even */
+  TURNKL_F32 = 1,
+} turnkl_dtype;
+
+/* Return codes. */
+typedef enum {
+  TURNKL_OK = 0,
+  TURNKL_ERR_INVALID_ARG = -1,   /* NULL, size, stride, dtype or alpha out of range */
+  TURNKL_ERR_ALIAS = -2,         /* grad_out overlaps an input other than exact in-place */
+  TURNKL_ERR_WORKSPACE = -3,     /* workspace smaller than turnkl_workspace_bytes() */
+  TURNKL_ERR_UNSORTED = -4,      /* device: trajectory or turn ids out of order */
+  TURNKL_ERR_TURN_RANGE = -5,    /* device: turn id outside [0, max_turns) */
+  TURNKL_ERR_PAD_MASK = -6,      /* device: padding token (traj_id < 0) with mask 1 */
+  TURNKL_ERR_HIP = -7,           /* a HIP runtime call failed */
+  TURNKL_ERR_SYNC_TIMEOUT = -8,  /* device: cross-workgroup exchange did not complete */
+} turnkl_status;
+
+/* Statistics of one turn index t over the supervised tokens at that turn. */
+typedef struct {
+  int64_t n_tokens;  /* supervised tokens at turn t, summed over trajectories */
+  int64_t n_traj;    /* trajectories with >= 1 supervised token at turn t (survivors n_t) */
+  double kl_mean;    /* pooled mean per-token KL at turn t (K_t); 0 if n_tokens == 0 */
+  double kl_m2;      /* sum over those tokens of (KL - kl_mean)^2 */
+  double kl_var;     /* kl_m2 / n_tokens (population variance); 0 if n_tokens == 0 */
+  double loss_mass;  /* sum over those tokens of w_i * KL_i (turn t's share of L) */
+} turnkl_turn_stat;
+
+/*
+ * Bytes of device workspace turnkl_fwd_bwd needs for this problem (host
+ * function, no device access).  Returns 0 when the arguments are invalid
+ * (n_tokens < 0, vocab < 1, unknown dtype, max_turns < 1).  The workspace
+ * needs no initialisation; it must be 256-byte aligned.
+ */
+size_t turnkl_workspace_bytes(int64_t n_tokens, int64_t vocab, int dtype, int32_t max_turns);
+
+/*
+ * Fused forward + backward of the turn-blended reverse-KL loss.
+ *
+ * student_logits, teacher_logits   [n_tokens x vocab] row-major, row strides
+ *                                  ld_student / ld_teacher (elements, >= vocab),
+ *                                  element type `dtype`.  Rows of unsupervised
+ *                                  tokens are never read.  Logits must be finite.
+ * turn_id, traj_id, loss_mask      [n_tokens] each.  A segment is a maximal run
+ *                                  of consecutive tokens with equal (traj_id,
+ *                                  turn_id); traj_id < 0 marks padding, which
+ *                                  belongs to no segment and must have mask 0.
+ *                                  Trajectory ids must increase from segment to
+ *                                  segment and turn ids must increase within a
+ *                                  trajectory (so a turn is one contiguous run);
+ *                                  0 <= turn_id < max_turns.  loss_mask[i] != 0
+ *                                  marks a supervised response token.
+ * alpha                            blend coefficient in [0, 1] (Sec. 5.2);
+ *                                  turnkl_alpha_schedule computes the paper's
+ *                                  schedule.
+ * grad_scale                       multiplies the gradient (the upstream
+ *                                  dLoss_total / dL); finite.
+ * loss_out                         [3] float: L_blend = sum_i w_i KL_i, L_traj
+ *                                  (alpha = 0) and L_turn (alpha = 1).  NaN x 3
+ *                                  when the device detects a data error.
+ * grad_out, ld_grad                [n_tokens x vocab] gradient in `dtype`, row
+ *                                  stride ld_grad >= vocab.  May equal
+ *                                  student_logits with ld_grad == ld_student
+ *                                  (in place); any other overlap with either
+ *                                  input is TURNKL_ERR_ALIAS.  Unsupervised rows
+ *                                  are written as zeros.  NULL: forward only.
+ * turn_stats_out, max_turns        [max_turns] statistics indexed by turn id, or
+ *                                  NULL.  accumulate_stats != 0 merges this
+ *                                  batch into the existing contents (counts and
+ *                                  loss mass add; means and m2 merge exactly as
+ *                                  if the tokens had been pooled); 0 overwrites.
+ * token_kl_out                     [n_tokens] float per-token KL (0 for
+ *                                  unsupervised tokens), or NULL.
+ * workspace, workspace_bytes       scratch of at least turnkl_workspace_bytes().
+ *
+ * Weights: w_i = m_i / B * ((1 - alpha) / N_b + alpha / (T_b * n_bt)) for token
+ * i of trajectory b at turn t, where n_bt is the supervised count of the
+ * segment, N_b = sum_t n_bt, T_b = #{t : n_bt > 0} and B = #{b : N_b > 0}; the
+ * weights sum to 1.  An empty batch or one without supervised tokens yields a
+ * zero loss, a zero gradient and zero (or unchanged, when accumulating) stats.
+ *
+ * Returns TURNKL_OK once everything is enqueued, or a negative host-detected
+ * error with nothing enqueued.  Device-detected data errors are reported by
+ * turnkl_get_status; after one, loss_out holds NaN and grad_out, turn_stats_out
+ * and token_kl_out are unspecified.
+ */
+int turnkl_fwd_bwd(const void* student_logits, int64_t ld_student, const void* teacher_logits,
+                   int64_t ld_teacher, int dtype, int64_t n_tokens, int64_t vocab,
+                   const int32_t* turn_id, const int32_t* traj_id, const uint8_t* loss_mask,
+                   double alpha, float grad_scale, float* loss_out, void* grad_out,
+                   int64_t ld_grad, turnkl_turn_stat* turn_stats_out, int32_t max_turns,
+                   int accumulate_stats, float* token_kl_out, void* workspace,
+                   size_t workspace_bytes, hipStream_t stream);
+
+/*
+ * Waits for `stream`, then returns the device-side status of the last
+ * turnkl_fwd_bwd call that used `workspace`: TURNKL_OK or a data error
+ * (TURNKL_ERR_UNSORTED / _TURN_RANGE / _PAD_MASK; the earliest offending token
+ * in token order decides, a range error before an ordering error on the same
+ * token), or TURNKL_ERR_SYNC_TIMEOUT; TURNKL_ERR_HIP if the read-back fails.
+ */
+int turnkl_get_status(const void* workspace, hipStream_t stream);
+
+/*
+ * Copies the segment table of the last call on `workspace` (made with the same
+ * n_tokens) into caller device arrays of capacity n_tokens: first token,
+ * length, trajectory id, turn id and supervised count of every segment, in
+ * token order.  *n_seg (host) receives the count.  Waits for `stream`.
+ * Returns TURNKL_OK, TURNKL_ERR_INVALID_ARG or TURNKL_ERR_HIP.
+ */
+int turnkl_get_segments(const void* workspace, int64_t n_tokens, hipStream_t stream,
+                        int32_t* n_seg, int32_t* seg_start, int32_t* seg_len, int32_t* seg_traj,
+                        int32_t* seg_turn, int32_t* seg_nsup);
+
+/*
+ * The paper's blend schedule (Sec. 5.2; App. D, Algorithm 1):
+ * alpha_k = clip((k / K - s) / (e - s), 0, 1).  When e <= s the schedule is a
+ * step: 1 once k / K >= s, else 0.  K < 1 returns NaN.  Host function.
+ */
+double turnkl_alpha_schedule(int64_t k, int64_t K, double s, double e);
+
+/* Static description of a return code.  Host function. */
+const char* turnkl_status_string(int status);
+
+/*
+ * Profiling hook for the calling host thread: while both events are non-NULL,
+ * every turnkl_fwd_bwd call made by this thread records `before` immediately
+ * before and `after` immediately after its row kernel (the kernel that reads
+ * the logits and writes the gradient), on the call's stream.  Pass NULL, NULL
+ * to stop.  The events must outlive the calls that record them.
+ */
+int turnkl_profile_row_kernel(hipEvent_t before, hipEvent_t after);
+
+/*
+ * Tiling override for the calling host thread.  The row kernel splits each
+ * row of V logits into ceil(V / (256 * e * n)) balanced chunks, one
+ * workgroup of 256 threads per chunk, where e is the number of elements in a
+ * 16-byte vector (8 bf16, 4 fp32) and n = vectors_per_thread is the most
+ * vectors a thread holds (1 to 16; default 16).  Smaller n means more, smaller
+ * chunks per row.  0 restores the default.  The workspace size depends on it
+ * (turnkl_workspace_bytes reads the same setting).  Results agree up to
+ * floating-point summation order.  Returns TURNKL_ERR_INVALID_ARG for values
+ * outside 0..16.
+ */
+int turnkl_set_row_tiling(int vectors_per_thread);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* TURNKL_H_ */

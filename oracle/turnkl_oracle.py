@@ -279,13 +279,13 @@ class Result:
 
 
 def fwd_bwd(traj_id, turn_id, loss_mask, alpha: float, max_turns: int, row_source,
-            vocab: int, dtype: int, grad_scale: float = 1.0, grad_rows=(),
-            chunk_rows: int = 256, n_threads: int = 0) -> Result:
+            dtype: int, grad_scale: float = 1.0, grad_rows=(), chunk_rows: int = 512,
+            n_threads: int = 0) -> Result:
     """Reference for one call of the fused path.
 
-    row_source(r0, r1) -> (zs, zt) host arrays for rows [r0, r1) (uint16 bf16
-    patterns or float32).  Only supervised rows are evaluated; rows listed in
-    grad_rows also return their gradient.
+    row_source(rows) -> (zs, zt): host arrays [len(rows), V] holding the
+    listed rows (uint16 bf16 patterns or float32).  Only supervised rows are
+    evaluated; rows listed in grad_rows also return their gradient.
     """
     traj_id = np.asarray(traj_id)
     loss_mask = np.asarray(loss_mask)
@@ -298,23 +298,18 @@ def fwd_bwd(traj_id, turn_id, loss_mask, alpha: float, max_turns: int, row_sourc
     w0 = token_weights(seg, n, loss_mask, 0.0)
     w1 = token_weights(seg, n, loss_mask, 1.0)
     kl = np.zeros(n, np.float64)
-    want = set(int(r) for r in grad_rows)
+    sup = np.nonzero(loss_mask)[0]
+    for k0 in range(0, sup.shape[0], chunk_rows):
+        rows = sup[k0:k0 + chunk_rows]
+        zs, zt = row_source(rows)
+        kl[rows], _ = row_kl(zs, zt, dtype, want_grad=False, n_threads=n_threads)
     grads = {}
-    for r0 in range(0, n, chunk_rows):
-        r1 = min(n, r0 + chunk_rows)
-        sup = np.nonzero(loss_mask[r0:r1])[0]
-        if sup.size == 0 and not want.intersection(range(r0, r1)):
-            continue
-        zs, zt = row_source(r0, r1)
-        rows = sorted(set(sup.tolist()) | {r - r0 for r in want if r0 <= r < r1})
-        need_g = [r for r in rows if r + r0 in want]
-        kls, _ = row_kl(zs[rows], zt[rows], dtype, want_grad=False, n_threads=n_threads)
-        for k, r in enumerate(rows):
-            if loss_mask[r0 + r]:
-                kl[r0 + r] = kls[k]
-        if need_g:
-            _, g = row_kl(zs[need_g], zt[need_g], dtype, want_grad=True, n_threads=n_threads)
-            for k, r in enumerate(need_g):
-                grads[r0 + r] = (g[k], grad_scale * w[r0 + r] * g[k])
+    want = np.asarray(sorted(set(int(r) for r in grad_rows)), np.int64)
+    for k0 in range(0, want.shape[0], chunk_rows):
+        rows = want[k0:k0 + chunk_rows]
+        zs, zt = row_source(rows)
+        _, g = row_kl(zs, zt, dtype, want_grad=True, n_threads=n_threads)
+        for k, r in enumerate(rows.tolist()):
+            grads[r] = (g[k], grad_scale * w[r] * g[k])
     stats = turn_stats([(seg, loss_mask, kl, w)], max_turns)
     return Result(OK, seg, w, kl, losses(w, w0, w1, kl), stats, grads)

@@ -1,0 +1,82 @@
+// Wave64 / workgroup reductions and scans with a fixed combination order, so
+// every result is reproducible bit for bit from run to run.
+#pragma once
+
+#include <hip/hip_runtime.h>
+
+namespace turnkl {
+
+constexpr int kWave = 64;
+
+template <typename T>
+__device__ inline T wave_sum(T v) {
+#pragma unroll
+  for (int o = kWave / 2; o > 0; o >>= 1) v += __shfl_xor(v, o, kWave);
+  return v;
+}
+
+template <typename T>
+__device__ inline T wave_max(T v) {
+#pragma unroll
+  for (int o = kWave / 2; o > 0; o >>= 1) v = fmaxf(v, __shfl_xor(v, o, kWave));
+  return v;
+}
+
+__device__ inline unsigned long long wave_min_u64(unsigned long long v) {
+#pragma unroll
+  for (int o = kWave / 2; o > 0; o >>= 1) {
+    const unsigned long long u = __shfl_xor(v, o, kWave);
+    v = u < v ? u : v;
+  }
+  return v;
+}
+
+// Inclusive prefix sum over the lanes of a wave.
+__device__ inline int wave_inclusive_scan(int v) {
+  const int lane = threadIdx.x & (kWave - 1);
+#pragma unroll
+  for (int o = 1; o < kWave; o <<= 1) {
+    const int u = __shfl_up(v, o, kWave);
+    if (lane >= o) v += u;
+  }
+  return v;
+}
+
+// Exclusive prefix sum over a workgroup of kThreads; *total gets the sum.
+// `lds` holds kThreads / 64 ints.  Contains two barriers.
+template <int kThreads>
+__device__ inline int block_exclusive_scan(int v, int* lds, int* total) {
+  constexpr int kWaves = kThreads / kWave;
+  const int lane = threadIdx.x & (kWave - 1);
+  const int wid = threadIdx.x / kWave;
+  const int inc = wave_inclusive_scan(v);
+  if (lane == kWave - 1) lds[wid] = inc;
+  __syncthreads();
+  int before = 0, all = 0;
+#pragma unroll
+  for (int w = 0; w < kWaves; ++w) {
+    const int x = lds[w];
+    before += (w < wid) ? x : 0;
+    all += x;
+  }
+  __syncthreads();
+  *total = all;
+  return before + inc - v;
+}
+
+// Sum over a workgroup, combined wave by wave in index order; every thread
+// receives the result.  `lds` holds kThreads / 64 values.  Two barriers.
+template <int kThreads, typename T>
+__device__ inline T block_sum(T v, T* lds) {
+  constexpr int kWaves = kThreads / kWave;
+  v = wave_sum(v);
+  if ((threadIdx.x & (kWave - 1)) == 0) lds[threadIdx.x / kWave] = v;
+  __syncthreads();
+  T s = lds[0];
+#pragma unroll
+  for (int w = 1; w < kWaves; ++w) s += lds[w];
+  __syncthreads();
+  return s;
+}
+
+}  // namespace turnkl

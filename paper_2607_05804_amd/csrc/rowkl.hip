@@ -1,0 +1,437 @@
+// Row kernel: per-token reverse KL over the full vocabulary and its gradient
+// with respect to the student logits, fused in one read of each logit.
+//
+// Math (Sec. 3, Eq. opd-rkl; teacher frozen; temperature 1).  For a row with
+// student logits a and teacher logits b:
+//   p_s = softmax(a),  mu = <p_s, a - b>,  lse = log sum exp
+//   KL  = mu - lse(a) + lse(b)
+//   dKL/da_v = p_s(v) (log p_s(v) - log p_t(v) - KL) = p_s(v) ((a_v - b_v) - mu)
+// so the gradient needs only lse(a) and mu, and the loss needs lse(b) too.
+// All exponentials are base 2 (v_exp_f32): a chunk keeps, in log2 units,
+//   M_s = max(a) log2(e),  S_s = sum 2^(a log2(e) - M_s),  A = sum 2^(...) (a - b),
+//   M_t = max(b) log2(e),  S_t = sum 2^(b log2(e) - M_t).
+//
+// Work decomposition.  A row of V elements (V / epv packs of 16 bytes) is cut
+// into n_chunks balanced chunks (pack counts differ by at most one); each of
+// a workgroup's 256 threads holds up to vpt packs.  One workgroup owns one
+// (row, chunk) task: it loads its chunk of both rows into registers, reduces
+// the five partials, publishes them as tagged 64-bit words, reads its row
+// mates' words, merges all chunks in chunk order (so every workgroup of the
+// row computes bit-identical row scalars), and writes its chunk of the
+// gradient straight from registers.  Every logit is read from HBM exactly
+// once and every gradient element written once: 3 V s bytes per supervised
+// row, V s per unsupervised row (zeros only).
+//
+// Tasks are handed out by an atomic ticket in row-major order, so a
+// workgroup only ever waits for tasks that running workgroups already hold
+// or that the next free workgroup will take; the wait is bounded and reports
+// TURNKL_ERR_SYNC_TIMEOUT instead of hanging.  An in-place gradient is safe
+// because each workgroup reads its chunk completely before writing it, and
+// chunks do not overlap.
+
+#include <hip/hip_bf16.h>
+
+#include "block_ops.h"
+#include "turnkl_internal.h"
+
+namespace turnkl {
+namespace {
+
+constexpr float kLog2e = 1.4426950408889634f;
+constexpr float kLn2 = 0.6931471805599453f;
+constexpr int kRowWaves = kRowThreads / kWave;
+constexpr int kSpinLimit = 1 << 22;
+
+// ---------------------------------------------------------------------------
+// packs of kEpv elements moved with one load/store
+
+// Buffer resource over one row chunk (gfx9 dword-3 word for raw dword
+// access).  The base is wave-uniform, so each pack's offset splits into a
+// per-lane VGPR part and a compile-time SGPR step.
+constexpr int kRsrcWord3 = 0x00020000;
+
+__device__ inline __amdgpu_buffer_rsrc_t chunk_rsrc(const void* base) {
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), 0, 0x7FFFFFFF, kRsrcWord3);
+}
+
+template <bool kBf16, int kEpv>
+struct Pack;
+
+template <>
+struct Pack<true, 8> {  // 8 bf16 = 16 bytes
+  unsigned w[4];
+  __device__ void load(__amdgpu_buffer_rsrc_t r, int voff, int soff) {
+    const auto u = __builtin_amdgcn_raw_buffer_load_b128(r, voff, soff, 0);
+    w[0] = u[0]; w[1] = u[1]; w[2] = u[2]; w[3] = u[3];
+  }
+  // Opaque to the optimiser: values unpacked before the fence cannot be
+  // reused after it, so only the packed words stay live between passes.
+  __device__ void fence() { asm volatile("" : "+v"(w[0]), "+v"(w[1]), "+v"(w[2]), "+v"(w[3])); }
+  __device__ float get(int j) const {
+    const unsigned x = w[j >> 1];
+    return __uint_as_float((j & 1) ? (x & 0xFFFF0000u) : (x << 16));
+  }
+  // flip = 0x80008000 negates both halves of every word
+  __device__ static void store(__amdgpu_buffer_rsrc_t r, int voff, int soff, const float (&g)[8],
+                               unsigned flip) {
+    __attribute__((ext_vector_type(4))) unsigned o;
+#pragma unroll
+    for (int k = 0; k < 4; ++k) {
+      const __hip_bfloat162 h = __float22bfloat162_rn(make_float2(g[2 * k], g[2 * k + 1]));
+      o[k] = *reinterpret_cast<const unsigned*>(&h) ^ flip;
+    }
+    __builtin_amdgcn_raw_buffer_store_b128(o, r, voff, soff, 0);
+  }
+  __device__ static void store_zero(__amdgpu_buffer_rsrc_t r, int voff, int soff) {
+    __attribute__((ext_vector_type(4))) unsigned o = {0u, 0u, 0u, 0u};
+    __builtin_amdgcn_raw_buffer_store_b128(o, r, voff, soff, 0);
+  }
+};
+
+template <>
+struct Pack<false, 4> {  // 4 fp32 = 16 bytes
+  float f[4];
+  __device__ void load(__amdgpu_buffer_rsrc_t r, int voff, int soff) {
+    const auto u = __builtin_amdgcn_raw_buffer_load_b128(r, voff, soff, 0);
+    f[0] = __uint_as_float(u[0]); f[1] = __uint_as_float(u[1]);
+    f[2] = __uint_as_float(u[2]); f[3] = __uint_as_float(u[3]);
+  }
+  __device__ void fence() { asm volatile("" : "+v"(f[0]), "+v"(f[1]), "+v"(f[2]), "+v"(f[3])); }
+  __device__ float get(int j) const { return f[j]; }
+  __device__ static void store(__amdgpu_buffer_rsrc_t r, int voff, int soff, const float (&g)[4],
+                               unsigned flip) {
+    const unsigned fl = flip << 16;  // sign bit of an fp32
+    __attribute__((ext_vector_type(4))) unsigned o;
+#pragma unroll
+    for (int k = 0; k < 4; ++k) o[k] = __float_as_uint(g[k]) ^ fl;
+    __builtin_amdgcn_raw_buffer_store_b128(o, r, voff, soff, 0);
+  }
+  __device__ static void store_zero(__amdgpu_buffer_rsrc_t r, int voff, int soff) {
+    __attribute__((ext_vector_type(4))) unsigned o = {0u, 0u, 0u, 0u};
+    __builtin_amdgcn_raw_buffer_store_b128(o, r, voff, soff, 0);
+  }
+};
+
+template <>
+struct Pack<true, 1> {  // one bf16
+  unsigned w;
+  __device__ void load(__amdgpu_buffer_rsrc_t r, int voff, int soff) {
+    w = __builtin_amdgcn_raw_buffer_load_b16(r, voff, soff, 0);
+  }
+  __device__ void fence() { asm volatile("" : "+v"(w)); }
+  __device__ float get(int) const { return __uint_as_float(w << 16); }
+  __device__ static void store(__amdgpu_buffer_rsrc_t r, int voff, int soff, const float (&g)[1],
+                               unsigned flip) {
+    const __hip_bfloat16 h = __float2bfloat16(g[0]);
+    const unsigned short bits =
+        (unsigned short)(*reinterpret_cast<const unsigned short*>(&h) ^ (flip & 0xFFFFu));
+    __builtin_amdgcn_raw_buffer_store_b16(bits, r, voff, soff, 0);
+  }
+  __device__ static void store_zero(__amdgpu_buffer_rsrc_t r, int voff, int soff) {
+    __builtin_amdgcn_raw_buffer_store_b16((unsigned short)0, r, voff, soff, 0);
+  }
+};
+
+template <>
+struct Pack<false, 1> {  // one fp32
+  float f;
+  __device__ void load(__amdgpu_buffer_rsrc_t r, int voff, int soff) {
+    f = __uint_as_float(__builtin_amdgcn_raw_buffer_load_b32(r, voff, soff, 0));
+  }
+  __device__ void fence() { asm volatile("" : "+v"(f)); }
+  __device__ float get(int) const { return f; }
+  __device__ static void store(__amdgpu_buffer_rsrc_t r, int voff, int soff, const float (&g)[1],
+                               unsigned flip) {
+    __builtin_amdgcn_raw_buffer_store_b32(__float_as_uint(g[0]) ^ (flip << 16), r, voff, soff, 0);
+  }
+  __device__ static void store_zero(__amdgpu_buffer_rsrc_t r, int voff, int soff) {
+    __builtin_amdgcn_raw_buffer_store_b32(0u, r, voff, soff, 0);
+  }
+};
+
+__device__ inline float exp2_fast(float x) { return __builtin_amdgcn_exp2f(x); }
+
+__device__ inline unsigned long long tagged(float v) {
+  return (1ull << 32) | (unsigned long long)__float_as_uint(v);
+}
+
+// One (row, chunk) task per iteration.  A chunk is the pack range
+// [pack_lo, pack_hi) of the row; thread tid owns packs pack_lo + v * 256 + tid
+// for v < kVpt.  With balanced chunks every pack v < kVpt - 1 lies inside the
+// chunk, so only the last one is predicated (kCheckAll: all of them, for the
+// unaligned scalar path whose chunk sizes are not balanced that way).
+template <bool kBf16, int kEpv, int kVpt, bool kCheckAll>
+__global__ __launch_bounds__(kRowThreads) void rowkl_kernel(RowParams p) {
+  using P = Pack<kBf16, kEpv>;
+  constexpr int kEs = kBf16 ? 2 : 4;
+  constexpr int kPackBytes = kEpv * kEs;
+  constexpr int kStep = kRowThreads * kPackBytes;  // bytes between a thread's packs
+
+  __shared__ float s_max[2][kRowWaves];
+  __shared__ float s_sum[3][kRowWaves];
+  __shared__ float s_part[kMaxPartialWords];
+  __shared__ unsigned s_task;
+  __shared__ int s_timeout;
+
+  if (p.hdr->err_key != kNoError) return;
+  const int tid = threadIdx.x;
+  const int lane = tid & (kWave - 1);
+  const int wid = tid / kWave;
+  const unsigned n_tasks = (unsigned)(p.n_rows * p.n_chunks);
+  const long long n_packs = p.vocab / kEpv;
+
+  for (;;) {
+    if (tid == 0) {
+      s_task = atomicAdd(&p.hdr->ticket, 1u);
+      s_timeout = 0;
+    }
+    __syncthreads();
+    const unsigned task = __builtin_amdgcn_readfirstlane(s_task);  // uniform: keep it scalar
+    if (task >= n_tasks) return;
+    const long long row = (long long)(task / (unsigned)p.n_chunks);
+    const int c = (int)(task - (unsigned)row * (unsigned)p.n_chunks);
+    const long long pack_lo = n_packs * c / p.n_chunks;
+    const long long pack_hi = n_packs * (c + 1) / p.n_chunks;
+    const int n_valid = (int)(pack_hi - pack_lo);  // packs in this chunk
+    const int lane_off = tid * kPackBytes;
+
+    bool valid[kVpt];
+#pragma unroll
+    for (int v = 0; v < kVpt; ++v)
+      valid[v] = (kCheckAll || v == kVpt - 1) ? (v * kRowThreads + tid < n_valid) : true;
+
+    if (!p.mask[row]) {
+      if (p.grad) {
+        const auto rg = chunk_rsrc(static_cast<char*>(p.grad) + (row * p.ld_g + pack_lo * kEpv) * kEs);
+#pragma unroll
+        for (int v = 0; v < kVpt; ++v)
+          if (valid[v]) P::store_zero(rg, lane_off, v * kStep);
+      }
+      __syncthreads();
+      continue;
+    }
+
+    // ---- load the chunk of both rows into registers (an out-of-chunk pack
+    // reads the chunk's first pack instead and is masked below)
+    const auto rs = chunk_rsrc(static_cast<const char*>(p.zs) + (row * p.ld_s + pack_lo * kEpv) * kEs);
+    const auto rt = chunk_rsrc(static_cast<const char*>(p.zt) + (row * p.ld_t + pack_lo * kEpv) * kEs);
+    P xs[kVpt], xt[kVpt];
+#pragma unroll
+    for (int v = 0; v < kVpt; ++v) {
+      const bool sure = !kCheckAll && v < kVpt - 1;
+      const int vo = sure ? lane_off : (valid[v] ? lane_off : 0);
+      const int so = sure ? v * kStep : (valid[v] ? v * kStep : 0);
+      xs[v].load(rs, vo, so);
+      xt[v].load(rt, vo, so);
+    }
+
+    // ---- chunk maxima
+    float ms = -INFINITY, mt = -INFINITY;
+#pragma unroll
+    for (int v = 0; v < kVpt; ++v) {
+#pragma unroll
+      for (int j = 0; j < kEpv; ++j) {
+        const float a = xs[v].get(j);
+        const float b = xt[v].get(j);
+        ms = fmaxf(ms, valid[v] ? a : -INFINITY);
+        mt = fmaxf(mt, valid[v] ? b : -INFINITY);
+      }
+    }
+    ms = wave_max(ms);
+    mt = wave_max(mt);
+    if (lane == 0) {
+      s_max[0][wid] = ms;
+      s_max[1][wid] = mt;
+    }
+    __syncthreads();
+    ms = s_max[0][0];
+    mt = s_max[1][0];
+#pragma unroll
+    for (int w = 1; w < kRowWaves; ++w) {
+      ms = fmaxf(ms, s_max[0][w]);
+      mt = fmaxf(mt, s_max[1][w]);
+    }
+    const float m2s = ms * kLog2e;
+    const float m2t = mt * kLog2e;
+#pragma unroll
+    for (int v = 0; v < kVpt; ++v) {
+      xs[v].fence();
+      xt[v].fence();
+    }
+
+    // ---- chunk sums
+    float ss = 0.0f, aa = 0.0f, st = 0.0f;
+#pragma unroll
+    for (int v = 0; v < kVpt; ++v) {
+#pragma unroll
+      for (int j = 0; j < kEpv; ++j) {
+        const float a = xs[v].get(j);
+        const float b = xt[v].get(j);
+        float es = exp2_fast(fmaf(a, kLog2e, -m2s));
+        float et = exp2_fast(fmaf(b, kLog2e, -m2t));
+        float d = a - b;
+        if (kCheckAll || v == kVpt - 1) {
+          es = valid[v] ? es : 0.0f;
+          et = valid[v] ? et : 0.0f;
+          d = valid[v] ? d : 0.0f;
+        }
+        ss += es;
+        aa = fmaf(es, d, aa);
+        st += et;
+      }
+    }
+    ss = wave_sum(ss);
+    aa = wave_sum(aa);
+    st = wave_sum(st);
+    if (lane == 0) {
+      s_sum[0][wid] = ss;
+      s_sum[1][wid] = aa;
+      s_sum[2][wid] = st;
+    }
+    __syncthreads();
+    ss = s_sum[0][0];
+    aa = s_sum[1][0];
+    st = s_sum[2][0];
+#pragma unroll
+    for (int w = 1; w < kRowWaves; ++w) {
+      ss += s_sum[0][w];
+      aa += s_sum[1][w];
+      st += s_sum[2][w];
+    }
+
+#pragma unroll
+    for (int v = 0; v < kVpt; ++v) {
+      xs[v].fence();
+      xt[v].fence();
+    }
+
+    // ---- row scalars: merge the chunks of the row in chunk order
+    float rm2s = m2s, rss = ss, raa = aa, rm2t = m2t, rst = st;
+    if (p.n_chunks > 1) {
+      const int nw = p.n_chunks * 5;
+      unsigned long long* slot = p.slots + row * (long long)nw;
+      if (tid == 0) {
+        unsigned long long* mine = slot + c * 5;
+        __hip_atomic_store(mine + 0, tagged(m2s), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        __hip_atomic_store(mine + 1, tagged(ss), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        __hip_atomic_store(mine + 2, tagged(aa), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        __hip_atomic_store(mine + 3, tagged(m2t), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        __hip_atomic_store(mine + 4, tagged(st), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      }
+      for (int q = tid; q < nw; q += kRowThreads) {
+        unsigned long long x;
+        int spins = 0;
+        while (((x = __hip_atomic_load(slot + q, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT)) >> 32) == 0ull) {
+          if (++spins > kSpinLimit) {
+            s_timeout = 1;
+            break;
+          }
+          __builtin_amdgcn_s_sleep(2);
+        }
+        s_part[q] = __uint_as_float((unsigned)x);
+      }
+      __syncthreads();
+      if (s_timeout) {
+        if (tid == 0) atomicMin(&p.hdr->err_key, err_key(0, kPrioTimeout));
+        return;
+      }
+      rm2s = -INFINITY;
+      rm2t = -INFINITY;
+      for (int k = 0; k < p.n_chunks; ++k) {
+        rm2s = fmaxf(rm2s, s_part[5 * k + 0]);
+        rm2t = fmaxf(rm2t, s_part[5 * k + 3]);
+      }
+      rss = 0.0f;
+      raa = 0.0f;
+      rst = 0.0f;
+      for (int k = 0; k < p.n_chunks; ++k) {
+        const float fs = exp2f(s_part[5 * k + 0] - rm2s);
+        const float ft = exp2f(s_part[5 * k + 3] - rm2t);
+        rss = fmaf(s_part[5 * k + 1], fs, rss);
+        raa = fmaf(s_part[5 * k + 2], fs, raa);
+        rst = fmaf(s_part[5 * k + 4], ft, rst);
+      }
+    }
+    const float mu = raa / rss;
+    if (c == 0 && tid == 0) p.kl[row] = mu + kLn2 * ((rm2t - rm2s) + log2f(rst / rss));
+
+    // ---- gradient chunk, straight from registers:
+    // G = grad_scale * w * 2^(a log2e - lse2_s) * ((a - b) - mu), with
+    // log2 |grad_scale * w| folded into the exponent and the sign applied last
+    if (p.grad) {
+      const float sc = p.wsc[row];
+      const float shift = (rm2s + log2f(rss)) - log2f(fabsf(sc));
+      const unsigned flip = sc < 0.0f ? 0x80008000u : 0u;
+      const auto rg = chunk_rsrc(static_cast<char*>(p.grad) + (row * p.ld_g + pack_lo * kEpv) * kEs);
+#pragma unroll
+      for (int v = 0; v < kVpt; ++v) {
+        float out[kEpv];
+#pragma unroll
+        for (int j = 0; j < kEpv; ++j) {
+          const float a = xs[v].get(j);
+          const float b = xt[v].get(j);
+          out[j] = exp2_fast(fmaf(a, kLog2e, -shift)) * ((a - b) - mu);
+        }
+        if (valid[v]) P::store(rg, lane_off, v * kStep, out, flip);
+      }
+    }
+    __syncthreads();
+  }
+}
+
+// ---------------------------------------------------------------------------
+// launch
+
+int cu_count() {
+  static int cache[64] = {0};
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0) return 256;
+  if (dev < 64 && cache[dev] > 0) return cache[dev];
+  int n = 0;
+  if (hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || n < 1) n = 256;
+  if (dev < 64) cache[dev] = n;
+  return n;
+}
+
+template <bool kBf16, int kEpv, int kVpt, bool kCheckAll>
+hipError_t launch_one(const RowParams& p, hipStream_t s) {
+  static const int occ = [] {
+    int n = 0;
+    if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&n, rowkl_kernel<kBf16, kEpv, kVpt, kCheckAll>,
+                                                     kRowThreads, 0) != hipSuccess || n < 1)
+      n = 1;
+    return n;
+  }();
+  const long long tasks = p.n_rows * (long long)p.n_chunks;
+  long long grid = (long long)occ * cu_count();
+  if (grid > tasks) grid = tasks;
+  if (grid < 1) return hipSuccess;
+  rowkl_kernel<kBf16, kEpv, kVpt, kCheckAll><<<dim3((unsigned)grid), dim3(kRowThreads), 0, s>>>(p);
+  return hipGetLastError();
+}
+
+template <bool kBf16, int kEpv>
+hipError_t launch_vpt(const RowParams& p, int vpt, hipStream_t s) {
+  switch (vpt) {
+#define TURNKL_CASE(n) \
+    case n: return launch_one<kBf16, kEpv, n, false>(p, s);
+    TURNKL_CASE(1) TURNKL_CASE(2) TURNKL_CASE(3) TURNKL_CASE(4) TURNKL_CASE(5) TURNKL_CASE(6)
+    TURNKL_CASE(7) TURNKL_CASE(8) TURNKL_CASE(9) TURNKL_CASE(10) TURNKL_CASE(11) TURNKL_CASE(12)
+    TURNKL_CASE(13) TURNKL_CASE(14) TURNKL_CASE(15) TURNKL_CASE(16)
+#undef TURNKL_CASE
+    default: return hipErrorInvalidValue;
+  }
+}
+
+}  // namespace
+
+hipError_t launch_rows(const RowParams& p, const RowTiling& t, hipStream_t s) {
+  if (p.n_rows == 0) return hipSuccess;
+  if (!t.vector) {
+    return p.bf16 ? launch_one<true, 1, kScalarVpt, true>(p, s)
+                  : launch_one<false, 1, kScalarVpt, true>(p, s);
+  }
+  return p.bf16 ? launch_vpt<true, 8>(p, t.vpt, s) : launch_vpt<false, 4>(p, t.vpt, s);
+}
+
+}  // namespace turnkl

@@ -1,0 +1,233 @@
+// Segment table, validation and token weights.
+//
+// A segment is a maximal run of consecutive tokens with equal (trajectory id,
+// turn id): turn t of a trace is its observation o_t followed by the response
+// r_t (Sec. 3), and the segment's supervised count is the paper's n_t for
+// that trajectory (Sec. 4.4).  The per-token weights follow the progressive
+// turn-normalised blend of Sec. 5.2 / App. D Algorithm 1 expanded per token:
+//   w_i = m_i / B * ((1 - alpha) / N_b + alpha / (T_b * n_bt)).
+//
+// Kernels, in launch order (all integer work is exact, so the table is unique):
+//   seg_count   per 1024-token tile: segment starts and the earliest id/mask
+//               error of the tile; clears the per-segment counters.
+//   seg_offsets one workgroup: exclusive scan of the tile counts, error key
+//               of the whole batch, header reset.
+//   seg_write   per tile: segment index of every token, segment start / turn /
+//               trajectory / end, supervised counts (integer atomics).
+//   seg_link    per segment: ordering check against the previous segment,
+//               segment length, trajectory head segment, T_b, N_b and B.
+//   token_weights per token: w_i and grad_scale * w_i, clears this call's
+//               per-token KL and the row kernel's exchange slots.
+
+#include "block_ops.h"
+#include "turnkl_internal.h"
+
+namespace turnkl {
+namespace {
+
+struct TokenInfo {
+  bool pad;
+  bool start;
+  unsigned long long err;
+};
+
+__device__ inline TokenInfo inspect(const SegParams& p, long long i) {
+  TokenInfo r{true, false, kNoError};
+  const int b = p.traj[i];
+  const int t = p.turn[i];
+  if (b < 0) {
+    if (p.mask[i]) r.err = err_key(i, kPrioPadMask);
+    return r;
+  }
+  r.pad = false;
+  if (t < 0 || t >= p.max_turns) r.err = err_key(i, kPrioTurnRange);
+  r.start = (i == 0) || p.traj[i - 1] != b || p.turn[i - 1] != t;
+  return r;
+}
+
+__global__ __launch_bounds__(kSegThreads) void seg_count(SegParams p, Ws ws) {
+  __shared__ int s_cnt[kSegThreads / kWave];
+  __shared__ unsigned long long s_err[kSegThreads / kWave];
+  const long long base = (long long)blockIdx.x * kSegTile + (long long)threadIdx.x * kSegTokensPerThread;
+  int cnt = 0;
+  unsigned long long err = kNoError;
+  for (int j = 0; j < kSegTokensPerThread; ++j) {
+    const long long i = base + j;
+    if (i >= p.n) break;
+    const TokenInfo ti = inspect(p, i);
+    cnt += ti.start ? 1 : 0;
+    err = ti.err < err ? ti.err : err;
+    ws.seg_nsup[i] = 0;
+    ws.traj_T[i] = 0;
+    ws.traj_N[i] = 0;
+  }
+  cnt = wave_sum(cnt);
+  err = wave_min_u64(err);
+  const int wid = threadIdx.x / kWave;
+  if ((threadIdx.x & (kWave - 1)) == 0) {
+    s_cnt[wid] = cnt;
+    s_err[wid] = err;
+  }
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    int c = 0;
+    unsigned long long e = kNoError;
+    for (int w = 0; w < kSegThreads / kWave; ++w) {
+      c += s_cnt[w];
+      e = s_err[w] < e ? s_err[w] : e;
+    }
+    ws.blk_cnt[blockIdx.x] = c;
+    ws.blk_err[blockIdx.x] = e;
+  }
+}
+
+constexpr int kScanThreads = 1024;
+
+__global__ __launch_bounds__(kScanThreads) void seg_offsets(Ws ws, long long nblk) {
+  __shared__ int s_scan[kScanThreads / kWave];
+  __shared__ unsigned long long s_err[kScanThreads / kWave];
+  int carry = 0;
+  unsigned long long err = kNoError;
+  for (long long b0 = 0; b0 < nblk; b0 += kScanThreads) {
+    const long long b = b0 + threadIdx.x;
+    const int v = b < nblk ? ws.blk_cnt[b] : 0;
+    if (b < nblk) err = ws.blk_err[b] < err ? ws.blk_err[b] : err;
+    int total;
+    const int ex = block_exclusive_scan<kScanThreads>(v, s_scan, &total);
+    if (b < nblk) ws.blk_off[b] = carry + ex;
+    carry += total;
+  }
+  err = wave_min_u64(err);
+  if ((threadIdx.x & (kWave - 1)) == 0) s_err[threadIdx.x / kWave] = err;
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    unsigned long long e = kNoError;
+    for (int w = 0; w < kScanThreads / kWave; ++w) e = s_err[w] < e ? s_err[w] : e;
+    ws.hdr->err_key = e;
+    ws.hdr->ticket = 0u;
+    ws.hdr->n_seg = carry;
+    ws.hdr->b_eff = 0;
+  }
+}
+
+__global__ __launch_bounds__(kSegThreads) void seg_write(SegParams p, Ws ws) {
+  __shared__ int s_scan[kSegThreads / kWave];
+  const long long base = (long long)blockIdx.x * kSegTile + (long long)threadIdx.x * kSegTokensPerThread;
+  TokenInfo ti[kSegTokensPerThread];
+  int cnt = 0;
+  for (int j = 0; j < kSegTokensPerThread; ++j) {
+    const long long i = base + j;
+    ti[j] = TokenInfo{true, false, kNoError};
+    if (i < p.n) ti[j] = inspect(p, i);
+    cnt += ti[j].start ? 1 : 0;
+  }
+  int total;
+  int seg = ws.blk_off[blockIdx.x] + block_exclusive_scan<kSegThreads>(cnt, s_scan, &total) - 1;
+  for (int j = 0; j < kSegTokensPerThread; ++j) {
+    const long long i = base + j;
+    if (i >= p.n) break;
+    if (ti[j].pad) {
+      ws.tok_seg[i] = -1;
+      continue;
+    }
+    if (ti[j].start) {
+      ++seg;
+      ws.seg_start[seg] = (int)i;
+      ws.seg_traj[seg] = p.traj[i];
+      ws.seg_turn[seg] = p.turn[i];
+    }
+    ws.tok_seg[i] = seg;
+    const bool last = (i + 1 == p.n) || p.traj[i + 1] != p.traj[i] || p.turn[i + 1] != p.turn[i];
+    if (last) ws.seg_len[seg] = (int)(i + 1);  // segment end; seg_link turns it into a length
+    if (p.mask[i]) atomicAdd(&ws.seg_nsup[seg], 1);
+  }
+}
+
+__global__ __launch_bounds__(kSegThreads) void seg_link(Ws ws) {
+  const int n_seg = ws.hdr->n_seg;
+  for (int s = blockIdx.x * kSegThreads + threadIdx.x; s < n_seg; s += gridDim.x * kSegThreads) {
+    const int b = ws.seg_traj[s];
+    const int t = ws.seg_turn[s];
+    const int start = ws.seg_start[s];
+    if (s > 0) {
+      const int pb = ws.seg_traj[s - 1];
+      const int pt = ws.seg_turn[s - 1];
+      if (b < pb || (b == pb && t <= pt)) atomicMin(&ws.hdr->err_key, err_key(start, kPrioUnsorted));
+    }
+    ws.seg_len[s] = ws.seg_len[s] - start;
+    // first segment of this trajectory (ids are sorted when the batch is valid)
+    int lo = 0, hi = s;
+    while (lo < hi) {
+      const int mid = (lo + hi) >> 1;
+      if (ws.seg_traj[mid] < b) lo = mid + 1; else hi = mid;
+    }
+    const int head = lo;
+    ws.seg_head[s] = head;
+    const int n = ws.seg_nsup[s];
+    if (n > 0) {
+      atomicAdd(&ws.traj_T[head], 1);
+      if (atomicAdd(&ws.traj_N[head], n) == 0) atomicAdd(&ws.hdr->b_eff, 1);
+    }
+  }
+}
+
+__global__ __launch_bounds__(kSegThreads) void token_weights(SegParams p, Ws ws, double alpha,
+                                                             float grad_scale, int slot_words,
+                                                             float* kl) {
+  if (ws.hdr->err_key != kNoError) return;
+  const double inv_b = ws.hdr->b_eff > 0 ? 1.0 / (double)ws.hdr->b_eff : 0.0;
+  for (long long i = (long long)blockIdx.x * kSegThreads + threadIdx.x; i < p.n;
+       i += (long long)gridDim.x * kSegThreads) {
+    kl[i] = 0.0f;
+    if (!p.mask[i]) {
+      ws.w[i] = 0.0f;
+      ws.wsc[i] = 0.0f;
+      continue;
+    }
+    const int s = ws.tok_seg[i];
+    const int h = ws.seg_head[s];
+    const double n_bt = (double)ws.seg_nsup[s];
+    const double t_b = (double)ws.traj_T[h];
+    const double n_b = (double)ws.traj_N[h];
+    const double w = inv_b * ((1.0 - alpha) / n_b + alpha / (t_b * n_bt));
+    ws.w[i] = (float)w;
+    ws.wsc[i] = (float)(w * (double)grad_scale);
+    if (slot_words) {
+      unsigned long long* sl = ws.slots + i * (long long)slot_words;
+      for (int q = 0; q < slot_words; ++q) sl[q] = 0ull;
+    }
+  }
+}
+
+int grid_for(long long items, int per_block, int cap) {
+  long long g = (items + per_block - 1) / per_block;
+  if (g < 1) g = 1;
+  return (int)(g < cap ? g : cap);
+}
+
+}  // namespace
+
+hipError_t launch_segments(const SegParams& p, const Ws& ws, long long nblk, hipStream_t s) {
+  if (nblk > 0) {
+    seg_count<<<dim3((unsigned)nblk), dim3(kSegThreads), 0, s>>>(p, ws);
+    if (hipError_t e = hipGetLastError(); e != hipSuccess) return e;
+  }
+  seg_offsets<<<1, kScanThreads, 0, s>>>(ws, nblk);
+  if (hipError_t e = hipGetLastError(); e != hipSuccess) return e;
+  if (nblk == 0) return hipSuccess;
+  seg_write<<<dim3((unsigned)nblk), dim3(kSegThreads), 0, s>>>(p, ws);
+  if (hipError_t e = hipGetLastError(); e != hipSuccess) return e;
+  seg_link<<<grid_for(p.n, kSegThreads, 1024), kSegThreads, 0, s>>>(ws);
+  return hipGetLastError();
+}
+
+hipError_t launch_weights(const SegParams& p, const Ws& ws, double alpha, float grad_scale,
+                          int n_chunks, float* kl, hipStream_t s) {
+  if (p.n == 0) return hipSuccess;
+  const int slot_words = n_chunks > 1 ? n_chunks * 5 : 0;
+  token_weights<<<grid_for(p.n, kSegThreads, 4096), kSegThreads, 0, s>>>(p, ws, alpha, grad_scale,
+                                                                         slot_words, kl);
+  return hipGetLastError();
+}
+
+}  // namespace turnkl

@@ -1,0 +1,239 @@
+// C-ABI of the fused turn-KL library: argument checks on the host, workspace
+// carve-up and the launch sequence (segments -> weights -> rows -> reduce),
+// all on the caller's stream with no host synchronisation.
+
+#include <math.h>
+#include <string.h>
+
+#include "turnkl_internal.h"
+
+namespace turnkl {
+
+namespace {
+thread_local hipEvent_t t_row_before = nullptr;
+thread_local hipEvent_t t_row_after = nullptr;
+thread_local int t_vpt_override = 0;
+
+bool vpt_allowed(int v) { return v >= 1 && v <= 16; }
+
+long long ceil_div(long long a, long long b) { return (a + b - 1) / b; }
+}  // namespace
+
+int thread_tiling_override() { return t_vpt_override; }
+
+// Balanced chunks: k = ceil(P / (256 * vmax)) chunks of P / k packs (P packs
+// per row), and vpt = ceil(ceil(P / k) / 256) packs per thread.  Then every
+// chunk holds at least 256 * (vpt - 1) packs, which the row kernel relies on
+// (only a thread's last pack can fall outside its chunk).
+RowTiling vector_tiling(long long vocab, int dtype, int vmax) {
+  RowTiling t{};
+  t.vector = true;
+  t.epv = dtype == TURNKL_BF16 ? 8 : 4;
+  if (vmax == 0) vmax = 16;
+  const long long packs = ceil_div(vocab, t.epv);
+  t.n_chunks = (int)ceil_div(packs, (long long)kRowThreads * vmax);
+  const long long widest = ceil_div(packs, t.n_chunks);
+  t.vpt = (int)ceil_div(widest, kRowThreads);
+  t.chunk = widest * t.epv;
+  return t;
+}
+
+RowTiling scalar_tiling(long long vocab) {
+  RowTiling t{};
+  t.vector = false;
+  t.epv = 1;
+  t.vpt = kScalarVpt;
+  t.n_chunks = (int)ceil_div(vocab, (long long)kRowThreads * kScalarVpt);
+  t.chunk = ceil_div(vocab, t.n_chunks);
+  return t;
+}
+
+namespace {
+
+// Exchange slots are sized for whichever path (vector or scalar) a call with
+// these sizes can take on this thread.
+int workspace_chunks(long long vocab, int dtype) {
+  const int a = vector_tiling(vocab, dtype, t_vpt_override).n_chunks;
+  const int b = scalar_tiling(vocab).n_chunks;
+  const int m = a > b ? a : b;
+  return m > 1 ? m : 0;
+}
+
+bool overlaps(const void* a, size_t na, const void* b, size_t nb) {
+  const char* pa = static_cast<const char*>(a);
+  const char* pb = static_cast<const char*>(b);
+  return pa < pb + nb && pb < pa + na;
+}
+
+size_t matrix_bytes(long long rows, long long ld, long long vocab, size_t es) {
+  return rows > 0 ? (size_t)((rows - 1) * ld + vocab) * es : 0;
+}
+
+}  // namespace
+}  // namespace turnkl
+
+using namespace turnkl;
+
+extern "C" {
+
+size_t turnkl_workspace_bytes(int64_t n_tokens, int64_t vocab, int dtype, int32_t max_turns) {
+  if (n_tokens < 0 || vocab < 1 || max_turns < 1) return 0;
+  if (dtype != TURNKL_BF16 && dtype != TURNKL_F32) return 0;
+  return make_layout(n_tokens, workspace_chunks(vocab, dtype)).total;
+}
+
+int turnkl_fwd_bwd(const void* student_logits, int64_t ld_student, const void* teacher_logits,
+                   int64_t ld_teacher, int dtype, int64_t n_tokens, int64_t vocab,
+                   const int32_t* turn_id, const int32_t* traj_id, const uint8_t* loss_mask,
+                   double alpha, float grad_scale, float* loss_out, void* grad_out,
+                   int64_t ld_grad, turnkl_turn_stat* turn_stats_out, int32_t max_turns,
+                   int accumulate_stats, float* token_kl_out, void* workspace,
+                   size_t workspace_bytes, hipStream_t stream) {
+  // ---- arguments
+  if (dtype != TURNKL_BF16 && dtype != TURNKL_F32) return TURNKL_ERR_INVALID_ARG;
+  if (n_tokens < 0 || n_tokens > 0x7FFFFFFFll || vocab < 1 || max_turns < 1)
+    return TURNKL_ERR_INVALID_ARG;
+  if (!(alpha >= 0.0 && alpha <= 1.0)) return TURNKL_ERR_INVALID_ARG;  // rejects NaN
+  if (!isfinite(grad_scale)) return TURNKL_ERR_INVALID_ARG;
+  if (!loss_out || !workspace) return TURNKL_ERR_INVALID_ARG;
+  if (n_tokens > 0) {
+    if (!student_logits || !teacher_logits || !turn_id || !traj_id || !loss_mask)
+      return TURNKL_ERR_INVALID_ARG;
+    if (ld_student < vocab || ld_teacher < vocab) return TURNKL_ERR_INVALID_ARG;
+    if (grad_out && ld_grad < vocab) return TURNKL_ERR_INVALID_ARG;
+  }
+  if (((uintptr_t)workspace & 255u) != 0) return TURNKL_ERR_WORKSPACE;
+
+  const size_t es = dtype == TURNKL_BF16 ? 2 : 4;
+  if (grad_out && n_tokens > 0) {
+    const size_t ng = matrix_bytes(n_tokens, ld_grad, vocab, es);
+    const size_t ns = matrix_bytes(n_tokens, ld_student, vocab, es);
+    const size_t nt = matrix_bytes(n_tokens, ld_teacher, vocab, es);
+    if (overlaps(grad_out, ng, teacher_logits, nt)) return TURNKL_ERR_ALIAS;
+    const bool in_place = grad_out == student_logits && ld_grad == ld_student;
+    if (!in_place && overlaps(grad_out, ng, student_logits, ns)) return TURNKL_ERR_ALIAS;
+  }
+
+  // ---- row tiling: 16-byte vectors when every row start is 16-byte aligned
+  RowTiling tiling = vector_tiling(vocab, dtype, t_vpt_override);
+  {
+    const long long epv = tiling.epv;
+    bool ok = vocab % epv == 0 && ld_student % epv == 0 && ld_teacher % epv == 0;
+    ok = ok && ((uintptr_t)student_logits & 15u) == 0 && ((uintptr_t)teacher_logits & 15u) == 0;
+    if (grad_out) ok = ok && ld_grad % epv == 0 && ((uintptr_t)grad_out & 15u) == 0;
+    const long long packs = vocab / epv;
+    ok = ok && packs / tiling.n_chunks >= (long long)kRowThreads * (tiling.vpt - 1);
+    if (!ok) tiling = scalar_tiling(vocab);
+  }
+  if (tiling.n_chunks * 5 > kMaxPartialWords) return TURNKL_ERR_INVALID_ARG;
+  if ((unsigned long long)n_tokens * (unsigned long long)tiling.n_chunks > 0x7FFFFFFFull)
+    return TURNKL_ERR_INVALID_ARG;
+
+  const Layout L = make_layout(n_tokens, workspace_chunks(vocab, dtype));
+  if (workspace_bytes < L.total) return TURNKL_ERR_WORKSPACE;
+  const Ws ws = bind(workspace, L);
+  float* kl = token_kl_out ? token_kl_out : ws.kl;
+
+  // ---- launches
+  const SegParams sp{traj_id, turn_id, loss_mask, (long long)n_tokens, max_turns};
+  if (launch_segments(sp, ws, L.nblk, stream) != hipSuccess) return TURNKL_ERR_HIP;
+  if (launch_weights(sp, ws, alpha, grad_scale, tiling.n_chunks, kl, stream) != hipSuccess)
+    return TURNKL_ERR_HIP;
+
+  RowParams rp{};
+  rp.zs = student_logits;
+  rp.ld_s = ld_student;
+  rp.zt = teacher_logits;
+  rp.ld_t = ld_teacher;
+  rp.grad = grad_out;
+  rp.ld_g = ld_grad;
+  rp.mask = loss_mask;
+  rp.wsc = ws.wsc;
+  rp.kl = kl;
+  rp.hdr = ws.hdr;
+  rp.slots = ws.slots;
+  rp.n_rows = n_tokens;
+  rp.vocab = vocab;
+  rp.n_chunks = tiling.n_chunks;
+  rp.bf16 = dtype == TURNKL_BF16;
+  const bool prof = t_row_before && t_row_after;
+  if (prof && hipEventRecord(t_row_before, stream) != hipSuccess) return TURNKL_ERR_HIP;
+  if (launch_rows(rp, tiling, stream) != hipSuccess) return TURNKL_ERR_HIP;
+  if (prof && hipEventRecord(t_row_after, stream) != hipSuccess) return TURNKL_ERR_HIP;
+
+  if (launch_reduce(sp, ws, kl, alpha, loss_out, turn_stats_out, accumulate_stats, stream) !=
+      hipSuccess)
+    return TURNKL_ERR_HIP;
+  return TURNKL_OK;
+}
+
+int turnkl_get_status(const void* workspace, hipStream_t stream) {
+  if (!workspace) return TURNKL_ERR_INVALID_ARG;
+  const Header* hdr = static_cast<const Header*>(workspace);
+  unsigned long long key = 0;
+  if (hipMemcpyAsync(&key, &hdr->err_key, sizeof key, hipMemcpyDeviceToHost, stream) != hipSuccess)
+    return TURNKL_ERR_HIP;
+  if (hipStreamSynchronize(stream) != hipSuccess) return TURNKL_ERR_HIP;
+  return status_from_key(key);
+}
+
+int turnkl_get_segments(const void* workspace, int64_t n_tokens, hipStream_t stream,
+                        int32_t* n_seg, int32_t* seg_start, int32_t* seg_len, int32_t* seg_traj,
+                        int32_t* seg_turn, int32_t* seg_nsup) {
+  if (!workspace || !n_seg || n_tokens < 0) return TURNKL_ERR_INVALID_ARG;
+  const Layout L = make_layout(n_tokens, 0);
+  const Ws ws = bind(const_cast<void*>(workspace), L);
+  int n = 0;
+  if (hipMemcpyAsync(&n, &ws.hdr->n_seg, sizeof n, hipMemcpyDeviceToHost, stream) != hipSuccess)
+    return TURNKL_ERR_HIP;
+  if (hipStreamSynchronize(stream) != hipSuccess) return TURNKL_ERR_HIP;
+  if (n < 0 || n > n_tokens) return TURNKL_ERR_INVALID_ARG;
+  *n_seg = n;
+  const size_t bytes = (size_t)n * 4;
+  struct { int32_t* dst; const int* src; } cp[] = {{seg_start, ws.seg_start}, {seg_len, ws.seg_len},
+                                                   {seg_traj, ws.seg_traj}, {seg_turn, ws.seg_turn},
+                                                   {seg_nsup, ws.seg_nsup}};
+  for (auto& c : cp) {
+    if (!c.dst || bytes == 0) continue;
+    if (hipMemcpyAsync(c.dst, c.src, bytes, hipMemcpyDeviceToDevice, stream) != hipSuccess)
+      return TURNKL_ERR_HIP;
+  }
+  return hipStreamSynchronize(stream) == hipSuccess ? TURNKL_OK : TURNKL_ERR_HIP;
+}
+
+double turnkl_alpha_schedule(int64_t k, int64_t K, double s, double e) {
+  if (K < 1) return NAN;
+  const double prog = (double)k / (double)K;
+  if (e <= s) return prog >= s ? 1.0 : 0.0;
+  const double a = (prog - s) / (e - s);
+  return a < 0.0 ? 0.0 : (a > 1.0 ? 1.0 : a);
+}
+
+const char* turnkl_status_string(int status) {
+  switch (status) {
+    case TURNKL_OK: return "ok";
+    case TURNKL_ERR_INVALID_ARG: return "invalid argument";
+    case TURNKL_ERR_ALIAS: return "grad_out overlaps an input";
+    case TURNKL_ERR_WORKSPACE: return "workspace too small or misaligned";
+    case TURNKL_ERR_UNSORTED: return "trajectory or turn ids out of order";
+    case TURNKL_ERR_TURN_RANGE: return "turn id outside [0, max_turns)";
+    case TURNKL_ERR_PAD_MASK: return "padding token with loss mask set";
+    case TURNKL_ERR_HIP: return "HIP runtime error";
+    case TURNKL_ERR_SYNC_TIMEOUT: return "row exchange timed out";
+    default: return "unknown status";
+  }
+}
+
+int turnkl_profile_row_kernel(hipEvent_t before, hipEvent_t after) {
+  t_row_before = before;
+  t_row_after = after;
+  return TURNKL_OK;
+}
+
+int turnkl_set_row_tiling(int vectors_per_thread) {
+  if (vectors_per_thread != 0 && !vpt_allowed(vectors_per_thread)) return TURNKL_ERR_INVALID_ARG;
+  t_vpt_override = vectors_per_thread;
+  return TURNKL_OK;
+}
+
+}  // extern "C"

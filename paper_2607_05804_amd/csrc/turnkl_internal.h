@@ -1,0 +1,206 @@
+// Internal declarations shared by the turnkl kernels and the C-ABI layer.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stddef.h>
+#include <stdint.h>
+
+#include "turnkl.h"
+
+namespace turnkl {
+
+// ---------------------------------------------------------------------------
+// error keys: the earliest offending token wins; at one token a padding-mask
+// error, then a turn-range error, then an ordering error.
+
+constexpr unsigned long long kNoError = ~0ull;
+enum : unsigned { kPrioPadMask = 0, kPrioTurnRange = 1, kPrioUnsorted = 2, kPrioTimeout = 3 };
+
+__host__ __device__ inline unsigned long long err_key(long long pos, unsigned prio) {
+  return ((unsigned long long)pos << 4) | prio;
+}
+
+inline int status_from_key(unsigned long long key) {
+  if (key == kNoError) return TURNKL_OK;
+  switch ((unsigned)(key & 0xF)) {
+    case kPrioPadMask: return TURNKL_ERR_PAD_MASK;
+    case kPrioTurnRange: return TURNKL_ERR_TURN_RANGE;
+    case kPrioUnsorted: return TURNKL_ERR_UNSORTED;
+    default: return TURNKL_ERR_SYNC_TIMEOUT;
+  }
+}
+
+// ---------------------------------------------------------------------------
+// workspace
+
+struct Header {
+  unsigned long long err_key;  // min over detected error keys; kNoError = none
+  unsigned int ticket;         // row-kernel work counter
+  int n_seg;                   // number of segments
+  int b_eff;                   // trajectories with >= 1 supervised token
+  int pad[59];
+};
+static_assert(sizeof(Header) == 256, "header is one 256-byte line");
+
+struct SegStat {
+  double sum;    // sum of KL over the segment's supervised tokens
+  double mean;   // sum / n
+  double m2;     // sum of (KL - mean)^2
+  double lm;     // w_seg * sum, the segment's share of L_blend
+  double ltraj;  // sum / (B * N_b), its share of L_traj
+  double lturn;  // sum / (B * T_b * n), its share of L_turn
+  long long n;   // supervised tokens
+  long long pad;
+};
+
+constexpr int kSegThreads = 256;
+constexpr int kSegTokensPerThread = 4;
+constexpr int kSegTile = kSegThreads * kSegTokensPerThread;
+
+// Byte offsets into the caller's workspace.  Everything up to and including
+// the segment table depends on n_tokens only (turnkl_get_segments relies on
+// that).
+struct Layout {
+  size_t header, blk_cnt, blk_off, blk_err, tok_seg, seg_start, seg_len, seg_traj, seg_turn,
+      seg_nsup, seg_head, traj_T, traj_N, w, wsc, kl, seg_stat, slots, total;
+  long long nblk;
+  int n_chunks;
+};
+
+inline size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
+
+inline Layout make_layout(long long n_tokens, int n_chunks) {
+  Layout L{};
+  const size_t n = (size_t)n_tokens;
+  L.nblk = (n_tokens + kSegTile - 1) / kSegTile;
+  L.n_chunks = n_chunks;
+  size_t o = 0;
+  auto take = [&](size_t bytes) { const size_t at = o; o = align256(o + bytes); return at; };
+  L.header = take(sizeof(Header));
+  L.blk_cnt = take((size_t)L.nblk * 4);
+  L.blk_off = take((size_t)L.nblk * 4);
+  L.blk_err = take((size_t)L.nblk * 8);
+  L.tok_seg = take(n * 4);
+  L.seg_start = take(n * 4);
+  L.seg_len = take(n * 4);
+  L.seg_traj = take(n * 4);
+  L.seg_turn = take(n * 4);
+  L.seg_nsup = take(n * 4);
+  L.seg_head = take(n * 4);
+  L.traj_T = take(n * 4);
+  L.traj_N = take(n * 4);
+  L.w = take(n * 4);
+  L.wsc = take(n * 4);
+  L.kl = take(n * 4);
+  L.seg_stat = take(n * sizeof(SegStat));
+  L.slots = take(n * (size_t)n_chunks * 5 * 8);
+  L.total = o;
+  return L;
+}
+
+// Device pointers into one workspace.
+struct Ws {
+  Header* hdr;
+  int* blk_cnt;
+  int* blk_off;
+  unsigned long long* blk_err;
+  int* tok_seg;
+  int* seg_start;
+  int* seg_len;
+  int* seg_traj;
+  int* seg_turn;
+  int* seg_nsup;
+  int* seg_head;
+  int* traj_T;
+  int* traj_N;
+  float* w;
+  float* wsc;
+  float* kl;
+  SegStat* seg_stat;
+  unsigned long long* slots;
+};
+
+inline Ws bind(void* base, const Layout& L) {
+  char* b = static_cast<char*>(base);
+  Ws w;
+  w.hdr = reinterpret_cast<Header*>(b + L.header);
+  w.blk_cnt = reinterpret_cast<int*>(b + L.blk_cnt);
+  w.blk_off = reinterpret_cast<int*>(b + L.blk_off);
+  w.blk_err = reinterpret_cast<unsigned long long*>(b + L.blk_err);
+  w.tok_seg = reinterpret_cast<int*>(b + L.tok_seg);
+  w.seg_start = reinterpret_cast<int*>(b + L.seg_start);
+  w.seg_len = reinterpret_cast<int*>(b + L.seg_len);
+  w.seg_traj = reinterpret_cast<int*>(b + L.seg_traj);
+  w.seg_turn = reinterpret_cast<int*>(b + L.seg_turn);
+  w.seg_nsup = reinterpret_cast<int*>(b + L.seg_nsup);
+  w.seg_head = reinterpret_cast<int*>(b + L.seg_head);
+  w.traj_T = reinterpret_cast<int*>(b + L.traj_T);
+  w.traj_N = reinterpret_cast<int*>(b + L.traj_N);
+  w.w = reinterpret_cast<float*>(b + L.w);
+  w.wsc = reinterpret_cast<float*>(b + L.wsc);
+  w.kl = reinterpret_cast<float*>(b + L.kl);
+  w.seg_stat = reinterpret_cast<SegStat*>(b + L.seg_stat);
+  w.slots = reinterpret_cast<unsigned long long*>(b + L.slots);
+  return w;
+}
+
+// ---------------------------------------------------------------------------
+// row-kernel tiling
+
+constexpr int kRowThreads = 256;
+constexpr int kScalarVpt = 32;         // elements per thread on the unaligned path
+constexpr int kMaxPartialWords = 640;  // LDS words for exchanged partials (n_chunks * 5)
+
+struct RowTiling {
+  bool vector;  // 16-byte vector loads (aligned rows, vocab a multiple of the vector)
+  int vpt;      // vectors (or scalar elements) per thread per chunk
+  int epv;      // elements per vector (8 bf16, 4 fp32, 1 on the scalar path)
+  long long chunk;  // elements of a row handled by one workgroup
+  int n_chunks;
+};
+
+// Tiling of the vector path for a given vectors-per-thread (0 = automatic).
+RowTiling vector_tiling(long long vocab, int dtype, int vpt);
+RowTiling scalar_tiling(long long vocab);
+int thread_tiling_override();
+
+// ---------------------------------------------------------------------------
+// launches (each returns hipSuccess or the launch error)
+
+struct SegParams {
+  const int* traj;
+  const int* turn;
+  const unsigned char* mask;
+  long long n;
+  int max_turns;
+};
+
+hipError_t launch_segments(const SegParams& p, const Ws& ws, long long nblk, hipStream_t s);
+hipError_t launch_weights(const SegParams& p, const Ws& ws, double alpha, float grad_scale,
+                          int n_chunks, float* kl, hipStream_t s);
+
+struct RowParams {
+  const void* zs;
+  long long ld_s;
+  const void* zt;
+  long long ld_t;
+  void* grad;
+  long long ld_g;
+  const unsigned char* mask;
+  const float* wsc;
+  float* kl;
+  Header* hdr;
+  unsigned long long* slots;
+  long long n_rows;
+  long long vocab;
+  int n_chunks;
+  int bf16;
+};
+
+hipError_t launch_rows(const RowParams& p, const RowTiling& t, hipStream_t s);
+
+hipError_t launch_reduce(const SegParams& p, const Ws& ws, const float* kl, double alpha,
+                         float* loss_out, turnkl_turn_stat* stats, int accumulate,
+                         hipStream_t s);
+
+}  // namespace turnkl

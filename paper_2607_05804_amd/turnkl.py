@@ -1,0 +1,219 @@
+"""Python binding of libturnkl.so: argument marshalling only.
+
+Every step of the fused turn-KL path runs in the library's HIP kernels; this
+module turns torch tensors into device pointers and the current HIP stream,
+calls the C ABI (include/turnkl.h) and raises on error.  It loads the
+in-tree library and fails loudly if it is missing; there is no fallback.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+
+import numpy as np
+import torch
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(HERE, "libturnkl.so")
+
+OK = 0
+ERR_INVALID_ARG = -1
+ERR_ALIAS = -2
+ERR_WORKSPACE = -3
+ERR_UNSORTED = -4
+ERR_TURN_RANGE = -5
+ERR_PAD_MASK = -6
+ERR_HIP = -7
+ERR_SYNC_TIMEOUT = -8
+
+BF16 = 0
+F32 = 1
+
+# Names of every entry point include/turnkl.h declares.
+EXPORTS = ("turnkl_workspace_bytes", "turnkl_fwd_bwd", "turnkl_get_status",
+           "turnkl_get_segments", "turnkl_alpha_schedule", "turnkl_status_string",
+           "turnkl_profile_row_kernel", "turnkl_set_row_tiling")
+
+STAT_DTYPE = np.dtype([("n_tokens", "<i8"), ("n_traj", "<i8"), ("kl_mean", "<f8"),
+                       ("kl_m2", "<f8"), ("kl_var", "<f8"), ("loss_mass", "<f8")])
+STAT_FIELDS = 6  # int64, int64, 4 x float64 -> 48 bytes
+
+_lib = None
+
+
+class TurnKLError(RuntimeError):
+    def __init__(self, code: int, what: str):
+        super().__init__(f"{what}: {status_string(code)} ({code})")
+        self.code = code
+
+
+def lib() -> ctypes.CDLL:
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIB_PATH):
+            raise RuntimeError(f"{LIB_PATH} is not built: run `python -c 'import __graft_entry__ as g; "
+                               "g.build()'` (no CPU fallback exists)")
+        l = ctypes.CDLL(LIB_PATH)
+        c = ctypes
+        l.turnkl_workspace_bytes.restype = c.c_size_t
+        l.turnkl_workspace_bytes.argtypes = [c.c_int64, c.c_int64, c.c_int, c.c_int32]
+        l.turnkl_fwd_bwd.restype = c.c_int
+        l.turnkl_fwd_bwd.argtypes = [
+            c.c_void_p, c.c_int64, c.c_void_p, c.c_int64, c.c_int, c.c_int64, c.c_int64,
+            c.c_void_p, c.c_void_p, c.c_void_p, c.c_double, c.c_float, c.c_void_p, c.c_void_p,
+            c.c_int64, c.c_void_p, c.c_int32, c.c_int, c.c_void_p, c.c_void_p, c.c_size_t,
+            c.c_void_p]
+        l.turnkl_get_status.restype = c.c_int
+        l.turnkl_get_status.argtypes = [c.c_void_p, c.c_void_p]
+        l.turnkl_get_segments.restype = c.c_int
+        l.turnkl_get_segments.argtypes = [c.c_void_p, c.c_int64, c.c_void_p,
+                                          c.POINTER(c.c_int32)] + [c.c_void_p] * 5
+        l.turnkl_alpha_schedule.restype = c.c_double
+        l.turnkl_alpha_schedule.argtypes = [c.c_int64, c.c_int64, c.c_double, c.c_double]
+        l.turnkl_status_string.restype = c.c_char_p
+        l.turnkl_status_string.argtypes = [c.c_int]
+        l.turnkl_profile_row_kernel.restype = c.c_int
+        l.turnkl_profile_row_kernel.argtypes = [c.c_void_p, c.c_void_p]
+        l.turnkl_set_row_tiling.restype = c.c_int
+        l.turnkl_set_row_tiling.argtypes = [c.c_int]
+        _lib = l
+    return _lib
+
+
+def status_string(code: int) -> str:
+    return lib().turnkl_status_string(code).decode()
+
+
+def alpha_schedule(k: int, K: int, s: float = 0.0, e: float = 1.0) -> float:
+    return float(lib().turnkl_alpha_schedule(k, K, s, e))
+
+
+def workspace_bytes(n_tokens: int, vocab: int, dtype: int, max_turns: int) -> int:
+    return int(lib().turnkl_workspace_bytes(n_tokens, vocab, dtype, max_turns))
+
+
+def set_row_tiling(vectors_per_thread: int) -> None:
+    rc = lib().turnkl_set_row_tiling(vectors_per_thread)
+    if rc != OK:
+        raise TurnKLError(rc, "turnkl_set_row_tiling")
+
+
+def profile_row_kernel(before, after) -> None:
+    """Record torch.cuda.Event objects around the row kernel of later calls (None, None: stop)."""
+    b = ctypes.c_void_p(before.cuda_event) if before is not None else None
+    a = ctypes.c_void_p(after.cuda_event) if after is not None else None
+    lib().turnkl_profile_row_kernel(b, a)
+
+
+def _dtype_code(t: torch.Tensor) -> int:
+    if t.dtype == torch.bfloat16:
+        return BF16
+    if t.dtype == torch.float32:
+        return F32
+    raise TypeError(f"logits must be bfloat16 or float32, got {t.dtype}")
+
+
+def _row_stride(t: torch.Tensor) -> int:
+    if t.dim() != 2 or t.stride(1) != 1:
+        raise ValueError("logits must be 2-D with unit column stride")
+    return int(t.stride(0)) if t.shape[0] > 1 else int(max(t.stride(0), t.shape[1]))
+
+
+def _ptr(t: torch.Tensor | None):
+    return None if t is None else ctypes.c_void_p(t.data_ptr())
+
+
+class Workspace:
+    """Caller-owned device scratch for turnkl_fwd_bwd (a uint8 torch tensor)."""
+
+    def __init__(self, n_tokens: int, vocab: int, dtype: int, max_turns: int, device="cuda"):
+        nbytes = workspace_bytes(n_tokens, vocab, dtype, max_turns)
+        if nbytes == 0:
+            raise TurnKLError(ERR_INVALID_ARG, "turnkl_workspace_bytes")
+        self.tensor = torch.empty(nbytes, dtype=torch.uint8, device=device)
+        self.nbytes = nbytes
+        self.n_tokens = n_tokens
+
+    def status(self) -> int:
+        stream = torch.cuda.current_stream().cuda_stream
+        return int(lib().turnkl_get_status(_ptr(self.tensor), ctypes.c_void_p(stream)))
+
+    def segments(self, device="cuda") -> dict:
+        n = self.n_tokens
+        bufs = [torch.empty(max(n, 1), dtype=torch.int32, device=device) for _ in range(5)]
+        n_seg = ctypes.c_int32(0)
+        stream = torch.cuda.current_stream().cuda_stream
+        rc = lib().turnkl_get_segments(_ptr(self.tensor), n, ctypes.c_void_p(stream),
+                                       ctypes.byref(n_seg), *[_ptr(b) for b in bufs])
+        if rc != OK:
+            raise TurnKLError(rc, "turnkl_get_segments")
+        k = n_seg.value
+        names = ("start", "length", "traj", "turn", "n_sup")
+        return {nm: b[:k].cpu().numpy().astype(np.int64) for nm, b in zip(names, bufs)}
+
+
+def fwd_bwd(student: torch.Tensor, teacher: torch.Tensor, turn_id: torch.Tensor,
+            traj_id: torch.Tensor, loss_mask: torch.Tensor, alpha: float, *,
+            grad_scale: float = 1.0, grad: str | torch.Tensor | None = "new",
+            max_turns: int = 64, turn_stats: torch.Tensor | None = None,
+            accumulate_stats: bool = False, token_kl: bool | torch.Tensor = False,
+            workspace: Workspace | None = None, check: bool = True):
+    """One fused forward + backward call on the current stream.
+
+    grad: "new" allocates the gradient, "inplace" writes it over `student`,
+    a tensor is used as the output, None computes the forward only.
+    turn_stats: optional [max_turns * 6] float64-compatible device buffer in
+    the turnkl_turn_stat layout (use new_turn_stats()); accumulate_stats
+    merges into it.  Returns (loss[3] tensor, grad or None, turn_stats or
+    None, token_kl or None, workspace).
+    """
+    dt = _dtype_code(student)
+    if teacher.dtype != student.dtype:
+        raise TypeError("student and teacher logits must share a dtype")
+    n, v = (int(student.shape[0]), int(student.shape[1])) if student.dim() == 2 else (0, 0)
+    for t in (turn_id, traj_id):
+        if t.dtype != torch.int32 or t.numel() != n:
+            raise ValueError("turn_id / traj_id must be int32 with one entry per row")
+    if loss_mask.dtype != torch.uint8 or loss_mask.numel() != n:
+        raise ValueError("loss_mask must be uint8 with one entry per row")
+    dev = student.device
+    if isinstance(grad, str):
+        if grad == "new":
+            grad_t = torch.empty_like(student)
+        elif grad == "inplace":
+            grad_t = student
+        else:
+            raise ValueError(grad)
+    else:
+        grad_t = grad
+    if workspace is None:
+        workspace = Workspace(n, v, dt, max_turns, device=dev)
+    loss = torch.empty(3, dtype=torch.float32, device=dev)
+    if isinstance(token_kl, torch.Tensor):
+        kl_t = token_kl
+    else:
+        kl_t = torch.empty(max(n, 1), dtype=torch.float32, device=dev) if token_kl else None
+    stream = torch.cuda.current_stream(dev).cuda_stream
+    rc = lib().turnkl_fwd_bwd(
+        _ptr(student), _row_stride(student) if n else v, _ptr(teacher),
+        _row_stride(teacher) if n else v, dt, n, v, _ptr(turn_id), _ptr(traj_id), _ptr(loss_mask),
+        float(alpha), float(grad_scale), _ptr(loss), _ptr(grad_t),
+        (_row_stride(grad_t) if n else v) if grad_t is not None else 0, _ptr(turn_stats),
+        int(max_turns), int(bool(accumulate_stats)), _ptr(kl_t), _ptr(workspace.tensor),
+        workspace.nbytes, ctypes.c_void_p(stream))
+    if rc != OK:
+        raise TurnKLError(rc, "turnkl_fwd_bwd")
+    if check:
+        st = workspace.status()
+        if st != OK:
+            raise TurnKLError(st, "turnkl_fwd_bwd (device)")
+    return loss, grad_t, turn_stats, kl_t, workspace
+
+
+def new_turn_stats(max_turns: int, device="cuda") -> torch.Tensor:
+    """Zeroed [max_turns] turnkl_turn_stat buffer (48 bytes each) as a uint8 tensor."""
+    return torch.zeros(max_turns * STAT_DTYPE.itemsize, dtype=torch.uint8, device=device)
+
+
+def read_turn_stats(buf: torch.Tensor) -> np.ndarray:
+    return buf.cpu().numpy().view(STAT_DTYPE)

@@ -39,6 +39,10 @@ def lib():
         l.synth_fill_host.argtypes = [ctypes.POINTER(SynthParams), ctypes.c_void_p,
                                       ctypes.c_int64, ctypes.c_int64, ctypes.c_void_p,
                                       ctypes.c_void_p, ctypes.c_int]
+        l.synth_fill_host_rows.restype = ctypes.c_int
+        l.synth_fill_host_rows.argtypes = [ctypes.POINTER(SynthParams), ctypes.c_void_p,
+                                           ctypes.c_void_p, ctypes.c_int64, ctypes.c_void_p,
+                                           ctypes.c_void_p, ctypes.c_int]
         _lib = l
     return _lib
 
@@ -54,6 +58,20 @@ def fill_host(params: SynthParams, teacher_scale: np.ndarray, r0: int, r1: int,
                                None if zt is None else zt.ctypes.data, n_threads)
     if rc != 0:
         raise RuntimeError(f"synth_fill_host failed ({rc})")
+
+
+def fill_host_rows(params: SynthParams, teacher_scale: np.ndarray, rows: np.ndarray,
+                   zs: np.ndarray | None, zt: np.ndarray | None, n_threads: int = 0) -> None:
+    """Write the listed rows (absolute indices) into consecutive rows of host arrays."""
+    if n_threads <= 0:
+        n_threads = min(16, os.cpu_count() or 1)
+    ts = np.ascontiguousarray(teacher_scale, dtype=np.float32)
+    r = np.ascontiguousarray(rows, dtype=np.int64)
+    rc = lib().synth_fill_host_rows(ctypes.byref(params), ts.ctypes.data, r.ctypes.data, r.shape[0],
+                                    None if zs is None else zs.ctypes.data,
+                                    None if zt is None else zt.ctypes.data, n_threads)
+    if rc != 0:
+        raise RuntimeError(f"synth_fill_host_rows failed ({rc})")
 
 
 def fill_device(params: SynthParams, teacher_scale_ptr: int, r0: int, r1: int,

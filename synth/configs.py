@@ -85,14 +85,12 @@ class Workload:
         return zs, zt
 
     def host_rows(self, rows, n_threads: int = 0):
-        """Arbitrary rows (any order) as host arrays, one generator call per row."""
-        rows = [int(r) for r in rows]
+        """Arbitrary rows (absolute indices, any order) as host arrays."""
+        rows = np.ascontiguousarray(rows, dtype=np.int64)
         dt = np.uint16 if self.dtype == BF16 else np.float32
-        zs = np.empty((len(rows), self.vocab), dtype=dt)
-        zt = np.empty((len(rows), self.vocab), dtype=dt)
-        for k, r in enumerate(rows):
-            _lib.fill_host(self.params(), self.teacher_scale, r, r + 1, zs[k:k + 1], zt[k:k + 1],
-                           n_threads)
+        zs = np.empty((rows.shape[0], self.vocab), dtype=dt)
+        zt = np.empty((rows.shape[0], self.vocab), dtype=dt)
+        _lib.fill_host_rows(self.params(), self.teacher_scale, rows, zs, zt, n_threads)
         return zs, zt
 
     def device_logits(self, ld: int | None = None, device: str = "cuda"):
@@ -212,15 +210,12 @@ def long_horizon(n_tokens: int = 65536) -> Workload:
     rng = np.random.default_rng(seed)
     lens: list[list[int]] = []
     total = 0
-    while total < n_tokens or len(lens) < 32:
-        if len(lens) >= 32 and total >= n_tokens:
-            break
+    # up to 32 trajectories, more only if they fall short of n_tokens
+    while total < n_tokens:
         t_b = int(rng.integers(20, 51))
         ls = np.clip(np.rint(rng.lognormal(4.0, 0.6, size=t_b)), 4, 512).astype(np.int64)
         lens.append([int(v) for v in ls])
         total += int(ls.sum())
-        if total >= n_tokens:
-            break
     # cut the packed batch at exactly n_tokens tokens
     traj, turn, mask = _pack(lens, [0.4] * len(lens))
     traj, turn, mask = traj[:n_tokens], turn[:n_tokens], mask[:n_tokens]

@@ -241,4 +241,33 @@ int synth_fill_host(const synth_params* p, const float* kt_host, int64_t r0, int
   return 0;
 }
 
+// Host rows listed in `rows` (n_rows absolute row indices, any order):
+// row rows[k] is written at zs_out / zt_out + k * p->ld elements.  Same bits
+// as the other fills.  Returns 0 or -1 on a bad argument.
+int synth_fill_host_rows(const synth_params* p, const float* kt_host, const int64_t* rows,
+                         int64_t n_rows, void* zs_out, void* zt_out, int n_threads) {
+  if (check_params(p, kt_host, 0, 0) || n_rows < 0 || (n_rows > 0 && !rows)) return -1;
+  if (n_rows == 0) return 0;
+  int nt = n_threads < 1 ? 1 : n_threads;
+  if ((int64_t)nt > n_rows) nt = (int)n_rows;
+  const size_t es = p->dtype == 0 ? 2 : 4;
+  std::vector<std::thread> pool;
+  for (int i = 0; i < nt; ++i) {
+    const int64_t ka = n_rows * i / nt;
+    const int64_t kb = n_rows * (i + 1) / nt;
+    pool.emplace_back([=] {
+      for (int64_t k = ka; k < kb; ++k) {
+        char* zs = zs_out ? static_cast<char*>(zs_out) + (size_t)k * (size_t)p->ld * es : nullptr;
+        char* zt = zt_out ? static_cast<char*>(zt_out) + (size_t)k * (size_t)p->ld * es : nullptr;
+        if (p->dtype == 0)
+          fill_rows_host<true>(*p, kt_host, rows[k], rows[k], rows[k] + 1, zs, zt);
+        else
+          fill_rows_host<false>(*p, kt_host, rows[k], rows[k], rows[k] + 1, zs, zt);
+      }
+    });
+  }
+  for (auto& t : pool) t.join();
+  return 0;
+}
+
 }  // extern "C"

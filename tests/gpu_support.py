@@ -1,0 +1,144 @@
+"""Helpers for the GPU parity tests: run the HIP path through the C ABI, run
+the CPU oracle on the same seeded inputs, and compare.
+
+Tolerances (derived in the design doc from the fp32 arithmetic of the kernels):
+  * segment table, counts, survivors, status codes: bit-exact;
+  * loss (each of L_blend, L_traj, L_turn): relative 1e-4;
+  * per-token KL: |d| <= 2e-4 |KL| + 5e-6;
+  * gradient, compared unweighted (g_hat = G / (grad_scale * w_i)):
+      |g_hat - g| <= 2e-2 absolute (the stated bar), and the tighter
+      |g_hat - g| <= 2^-8 |g| + 2e-5 for bf16 output (about one bf16 ulp),
+      |g_hat - g| <= 1e-4 |g| + 2e-6 for fp32 output;
+    unsupervised rows must be exactly zero;
+  * per-turn stats: mean and loss mass relative 1e-4, variance
+    |d| <= 1e-4 var + 1e-8.
+"""
+from __future__ import annotations
+
+import sys
+
+import numpy as np
+import torch
+
+from oracle import turnkl_oracle as O
+from paper_2607_05804_amd import turnkl as T
+
+
+def log(msg: str) -> None:
+    print(msg, flush=True)
+    sys.stdout.flush()
+
+
+def to_device_logits(arr: np.ndarray, device="cuda") -> torch.Tensor:
+    """Host logits (uint16 bf16 patterns or float32) -> device tensor."""
+    if arr.dtype == np.uint16:
+        return torch.from_numpy(arr.view(np.int16)).to(device).view(torch.bfloat16)
+    return torch.from_numpy(arr).to(device)
+
+
+def rows_to_host(t: torch.Tensor, rows) -> np.ndarray:
+    """Selected rows of a device bf16/fp32 matrix as float32 on the host."""
+    idx = torch.as_tensor(np.asarray(rows, np.int64), device=t.device)
+    sel = t.index_select(0, idx)
+    if sel.dtype == torch.bfloat16:
+        u = sel.contiguous().view(torch.int16).cpu().numpy().view(np.uint16)
+        return (u.astype(np.uint32) << 16).view(np.float32)
+    return sel.float().cpu().numpy()
+
+
+def oracle_dtype(dtype: torch.dtype) -> int:
+    return O.DTYPE_BF16 if dtype == torch.bfloat16 else O.DTYPE_F32
+
+
+def ids_to_device(traj, turn, mask, device="cuda"):
+    return (torch.from_numpy(np.ascontiguousarray(turn, np.int32)).to(device),
+            torch.from_numpy(np.ascontiguousarray(traj, np.int32)).to(device),
+            torch.from_numpy(np.ascontiguousarray(mask, np.uint8)).to(device))
+
+
+def check_segments(ws: T.Workspace, ref: O.Segments) -> None:
+    got = ws.segments()
+    assert len(got["start"]) == ref.count, (len(got["start"]), ref.count)
+    for k in ("start", "length", "traj", "turn", "n_sup"):
+        assert np.array_equal(got[k], getattr(ref, k)), k
+
+
+def check_loss(loss: torch.Tensor, ref_loss, rtol=1e-4) -> None:
+    got = loss.cpu().numpy().astype(np.float64)
+    for g, r, name in zip(got, ref_loss, ("L_blend", "L_traj", "L_turn")):
+        assert abs(g - r) <= rtol * abs(r) + 1e-12, (name, g, r, abs(g - r) / max(abs(r), 1e-30))
+
+
+def check_token_kl(kl_dev: torch.Tensor, ref_kl: np.ndarray, mask: np.ndarray) -> None:
+    got = kl_dev.cpu().numpy()[: ref_kl.shape[0]].astype(np.float64)
+    err = np.abs(got - ref_kl)
+    bound = 2e-4 * np.abs(ref_kl) + 5e-6
+    bad = np.nonzero(err > bound)[0]
+    assert bad.size == 0, (bad[:5], got[bad[:5]], ref_kl[bad[:5]])
+    assert np.all(got[np.asarray(mask) == 0] == 0.0)
+
+
+def check_stats(stats_buf: torch.Tensor, ref: np.ndarray) -> None:
+    got = T.read_turn_stats(stats_buf)
+    assert np.array_equal(got["n_tokens"], ref["n_tokens"])
+    assert np.array_equal(got["n_traj"], ref["n_traj"])
+    for f in ("kl_mean", "loss_mass"):
+        err = np.abs(got[f] - ref[f])
+        assert np.all(err <= 1e-4 * np.abs(ref[f]) + 1e-12), (f, np.max(err))
+    err = np.abs(got["kl_var"] - ref["kl_var"])
+    assert np.all(err <= 1e-4 * ref["kl_var"] + 1e-8), ("kl_var", np.max(err))
+    err = np.abs(got["kl_m2"] - ref["kl_m2"])
+    assert np.all(err <= 1e-4 * ref["kl_m2"] + 1e-8 * np.maximum(ref["n_tokens"], 1)), \
+        ("kl_m2", np.max(err))
+
+
+def check_grad_rows(grad_dev: torch.Tensor, ref: O.Result, grad_scale: float, rows,
+                    mask: np.ndarray) -> float:
+    """Compare gradient rows; returns the worst unweighted absolute error."""
+    rows = list(rows)
+    G = rows_to_host(grad_dev, rows).astype(np.float64)
+    bf16 = grad_dev.dtype == torch.bfloat16
+    worst = 0.0
+    for k, r in enumerate(rows):
+        if not mask[r]:
+            assert np.all(G[k] == 0.0), ("unsupervised row not zero", r)
+            continue
+        g_ref = ref.grads[r][0]
+        scale = grad_scale * ref.w[r]
+        g_hat = G[k] / scale
+        err = np.abs(g_hat - g_ref)
+        worst = max(worst, float(err.max()))
+        assert err.max() <= 2e-2, (r, err.max())
+        bound = (2.0 ** -8 * np.abs(g_ref) + 2e-5) if bf16 else (1e-4 * np.abs(g_ref) + 2e-6)
+        bad = np.nonzero(err > bound)[0]
+        assert bad.size == 0, (r, bad[:5], g_hat[bad[:5]], g_ref[bad[:5]])
+    return worst
+
+
+def sample_rows(mask: np.ndarray, n_sup: int = 24, n_unsup: int = 4, seed: int = 0):
+    """First, last and random supervised rows, plus a few unsupervised ones."""
+    rng = np.random.default_rng(seed)
+    sup = np.nonzero(mask)[0]
+    uns = np.nonzero(np.asarray(mask) == 0)[0]
+    pick = set()
+    if sup.size:
+        pick |= {int(sup[0]), int(sup[-1])}
+        pick |= set(int(x) for x in rng.choice(sup, size=min(n_sup, sup.size), replace=False))
+    if uns.size:
+        pick |= set(int(x) for x in rng.choice(uns, size=min(n_unsup, uns.size), replace=False))
+    return sorted(pick)
+
+
+def rows_bits_to_host(t: torch.Tensor, rows) -> np.ndarray:
+    """Selected rows of a device matrix in the oracle's input format
+    (uint16 bf16 patterns, or float32)."""
+    idx = torch.as_tensor(np.asarray(rows, np.int64), device=t.device)
+    sel = t.index_select(0, idx).contiguous()
+    if sel.dtype == torch.bfloat16:
+        return sel.view(torch.int16).cpu().numpy().view(np.uint16)
+    return sel.cpu().numpy()
+
+
+def device_row_source(zs: torch.Tensor, zt: torch.Tensor):
+    """Oracle row source reading the generator's output from device memory."""
+    return lambda rows: (rows_bits_to_host(zs, rows), rows_bits_to_host(zt, rows))

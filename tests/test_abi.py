@@ -1,0 +1,124 @@
+"""The C-ABI library loads, exports what include/turnkl.h declares, and rejects
+bad arguments on the host before anything is enqueued (no GPU needed: every
+call here returns before the first HIP runtime call)."""
+import ctypes
+import os
+import re
+
+import pytest
+
+from paper_2607_05804_amd import turnkl as T
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "turnkl.h")
+
+
+def declared_functions():
+    src = open(HEADER).read()
+    src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
+    return sorted(set(re.findall(r"\b(turnkl_[a-z_]+)\s*\(", src)))
+
+
+def test_every_declared_symbol_is_exported():
+    names = declared_functions()
+    assert set(names) == set(T.EXPORTS), names
+    lib = ctypes.CDLL(T.LIB_PATH)
+    for n in names:
+        assert hasattr(lib, n), n
+
+
+def test_status_strings_and_alpha_schedule():
+    assert T.status_string(T.OK) == "ok"
+    for code in range(-8, 0):
+        assert T.status_string(code) != "unknown status"
+    assert T.status_string(-99) == "unknown status"
+    assert T.alpha_schedule(0, 100) == 0.0
+    assert T.alpha_schedule(50, 100) == 0.5
+    assert T.alpha_schedule(150, 100) == 1.0
+    assert T.alpha_schedule(3, 10, 0.2, 0.6) == pytest.approx(0.25)
+    assert T.alpha_schedule(5, 10, 0.6, 0.6) == 0.0 and T.alpha_schedule(6, 10, 0.6, 0.6) == 1.0
+    import math
+    assert math.isnan(T.alpha_schedule(1, 0))
+
+
+def test_workspace_bytes():
+    assert T.workspace_bytes(-1, 10, T.BF16, 4) == 0
+    assert T.workspace_bytes(10, 0, T.BF16, 4) == 0
+    assert T.workspace_bytes(10, 10, 7, 4) == 0
+    assert T.workspace_bytes(10, 10, T.BF16, 0) == 0
+    a = T.workspace_bytes(1000, 151936, T.BF16, 50)
+    b = T.workspace_bytes(2000, 151936, T.BF16, 50)
+    assert 0 < a < b and a % 256 == 0
+    assert T.workspace_bytes(0, 10, T.F32, 1) > 0
+    # smaller per-thread tiles mean more chunks per row and more exchange slots
+    T.set_row_tiling(1)
+    try:
+        c = T.workspace_bytes(1000, 151936, T.BF16, 50)
+    finally:
+        T.set_row_tiling(0)
+    assert c > a
+    with pytest.raises(T.TurnKLError):
+        T.set_row_tiling(17)
+    with pytest.raises(T.TurnKLError):
+        T.set_row_tiling(-1)
+
+
+def _call(**kw):
+    """turnkl_fwd_bwd with fake (never dereferenced) addresses unless overridden."""
+    n, v = kw.get("n", 64), kw.get("v", 1024)
+    es = 2 if kw.get("dtype", T.BF16) == T.BF16 else 4
+    zs = kw.get("zs", 0x100000000)
+    zt = kw.get("zt", 0x200000000)
+    ws_bytes = T.workspace_bytes(n, v, kw.get("dtype", T.BF16), kw.get("max_turns", 8))
+    args = dict(zs=zs, ld_s=v, zt=zt, ld_t=v, dtype=T.BF16, n=n, v=v, turn=0x300000000,
+                traj=0x300100000, mask=0x300200000, alpha=0.5, scale=1.0, loss=0x300300000,
+                grad=0x400000000, ld_g=v, stats=0, max_turns=8, acc=0, kl=0,
+                ws=0x500000000, ws_bytes=ws_bytes)
+    args.update(kw)
+    p = lambda x: ctypes.c_void_p(x) if x else None
+    return T.lib().turnkl_fwd_bwd(
+        p(args["zs"]), args["ld_s"], p(args["zt"]), args["ld_t"], args["dtype"], args["n"],
+        args["v"], p(args["turn"]), p(args["traj"]), p(args["mask"]), args["alpha"],
+        args["scale"], p(args["loss"]), p(args["grad"]), args["ld_g"], p(args["stats"]),
+        args["max_turns"], args["acc"], p(args["kl"]), p(args["ws"]), args["ws_bytes"], None)
+
+
+@pytest.mark.parametrize("kw,code", [
+    (dict(dtype=5), T.ERR_INVALID_ARG),
+    (dict(n=-1), T.ERR_INVALID_ARG),
+    (dict(v=0), T.ERR_INVALID_ARG),
+    (dict(max_turns=0), T.ERR_INVALID_ARG),
+    (dict(alpha=-0.1), T.ERR_INVALID_ARG),
+    (dict(alpha=1.5), T.ERR_INVALID_ARG),
+    (dict(alpha=float("nan")), T.ERR_INVALID_ARG),
+    (dict(scale=float("inf")), T.ERR_INVALID_ARG),
+    (dict(scale=float("nan")), T.ERR_INVALID_ARG),
+    (dict(loss=0), T.ERR_INVALID_ARG),
+    (dict(ws=0), T.ERR_INVALID_ARG),
+    (dict(zs=0), T.ERR_INVALID_ARG),
+    (dict(zt=0), T.ERR_INVALID_ARG),
+    (dict(turn=0), T.ERR_INVALID_ARG),
+    (dict(traj=0), T.ERR_INVALID_ARG),
+    (dict(mask=0), T.ERR_INVALID_ARG),
+    (dict(ld_s=1023), T.ERR_INVALID_ARG),
+    (dict(ld_t=1000), T.ERR_INVALID_ARG),
+    (dict(ld_g=1), T.ERR_INVALID_ARG),
+    # gradient overlapping the teacher, or the student other than exactly in place
+    (dict(grad=0x200000000), T.ERR_ALIAS),
+    (dict(grad=0x200000000 + 64 * 1024), T.ERR_ALIAS),
+    (dict(grad=0x100000000 + 2), T.ERR_ALIAS),
+    (dict(grad=0x100000000, ld_g=2048), T.ERR_ALIAS),
+    (dict(grad=0x100000000 - 2 * 1024), T.ERR_ALIAS),
+    # workspace too small or misaligned
+    (dict(ws_bytes=1024), T.ERR_WORKSPACE),
+    (dict(ws=0x500000010), T.ERR_WORKSPACE),
+])
+def test_host_rejects_bad_arguments_before_launch(kw, code):
+    assert _call(**kw) == code
+
+
+def test_binding_fails_loudly_without_library(monkeypatch, tmp_path):
+    monkeypatch.setattr(T, "_lib", None)
+    monkeypatch.setattr(T, "LIB_PATH", str(tmp_path / "missing.so"))
+    with pytest.raises(RuntimeError, match="not built"):
+        T.lib()

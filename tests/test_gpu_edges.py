@@ -1,0 +1,350 @@
+"""Edge cases, tilings, error paths and invariants of the HIP path, each
+checked against the CPU oracle (or an exact property) through the C ABI."""
+import numpy as np
+import pytest
+import torch
+
+from gpu_support import (check_grad_rows, check_loss, check_segments, check_stats,
+                         check_token_kl, ids_to_device, log, to_device_logits)
+from oracle import turnkl_oracle as O
+from paper_2607_05804_amd import turnkl as T
+
+pytestmark = pytest.mark.gpu
+
+
+def bf16_bits(x):
+    u = np.asarray(x, np.float32).view(np.uint32).astype(np.uint64)
+    return ((u + 0x7FFF + ((u >> 16) & 1)) >> 16).astype(np.uint16)
+
+
+def make_batch(seed, n_traj=5, max_turns=6, V=1000, dtype="bf16", pad=True, sigma=3.0,
+               noise=1.0, min_len=1, max_len=40):
+    rng = np.random.default_rng(seed)
+    traj, turn, mask = [], [], []
+    for b in range(n_traj):
+        turns = np.sort(rng.choice(max_turns, size=int(rng.integers(1, max_turns + 1)),
+                                   replace=False))
+        for t in turns:
+            n = int(rng.integers(min_len, max_len + 1))
+            if pad and rng.uniform() < 0.2:
+                k = int(rng.integers(1, 4))
+                traj += [-1] * k
+                turn += [0] * k
+                mask += [0] * k
+            traj += [b] * n
+            turn += [int(t)] * n
+            mode = int(rng.integers(0, 4))
+            if mode == 0:
+                mask += [0] * n
+            elif mode == 1:
+                mask += [1] * n
+            else:
+                o = n * 2 // 5
+                mask += [0] * o + [1] * (n - o)
+    traj = np.array(traj, np.int32)
+    turn = np.array(turn, np.int32)
+    mask = np.array(mask, np.uint8)
+    zs = rng.normal(0.0, sigma, (len(traj), V)).astype(np.float32)
+    zt = (zs + rng.normal(0.0, noise, zs.shape)).astype(np.float32)
+    if dtype == "bf16":
+        zs, zt = bf16_bits(zs), bf16_bits(zt)
+    return traj, turn, mask, zs, zt
+
+
+def run_both(traj, turn, mask, zs_h, zt_h, alpha=0.4, max_turns=8, grad_scale=1.0, ld=None,
+             grad="new", grad_rows=None, vpt=0):
+    dev = "cuda"
+    n, V = zs_h.shape
+    if ld is None:
+        zs, zt = to_device_logits(zs_h, dev), to_device_logits(zt_h, dev)
+    else:  # padded row stride; the padding holds NaN and must never be read
+        def padded(h):
+            full = np.full((n, ld), np.nan, np.float32)
+            d = to_device_logits(full.astype(np.float32), dev)
+            if h.dtype == np.uint16:
+                d = d.to(torch.bfloat16)
+            d[:, :V] = to_device_logits(h, dev)
+            return d[:, :V]
+        zs, zt = padded(zs_h), padded(zt_h)
+    turn_d, traj_d, mask_d = ids_to_device(traj, turn, mask, dev)
+    stats = T.new_turn_stats(max_turns)
+    T.set_row_tiling(vpt)
+    try:
+        loss, g, _, kl, ws = T.fwd_bwd(zs, zt, turn_d, traj_d, mask_d, alpha, grad_scale=grad_scale,
+                                       grad=grad, max_turns=max_turns, turn_stats=stats,
+                                       token_kl=True)
+    finally:
+        T.set_row_tiling(0)
+    torch.cuda.synchronize()
+    rows = list(range(n)) if grad_rows is None else grad_rows
+    dt = O.DTYPE_BF16 if zs_h.dtype == np.uint16 else O.DTYPE_F32
+    ref = O.fwd_bwd(traj, turn, mask, alpha, max_turns, lambda r: (zs_h[r], zt_h[r]), dt,
+                    grad_scale, rows)
+    return (loss, g, stats, kl, ws), ref, rows
+
+
+def check_all(out, ref, mask, grad_scale, rows):
+    loss, g, stats, kl, ws = out
+    check_segments(ws, ref.seg)
+    check_loss(loss, ref.loss)
+    check_token_kl(kl, ref.kl, mask)
+    check_stats(stats, ref.stats)
+    if g is not None:
+        check_grad_rows(g, ref, grad_scale, rows, mask)
+
+
+# ----------------------------------------------------------------------------
+# tilings and vocabulary shapes
+
+
+@pytest.mark.parametrize("V,dtype,vpt", [
+    (1024, "f32", 0), (1024, "f32", 1),            # one chunk / four chunks per row
+    (32000, "bf16", 0), (32000, "bf16", 1), (32000, "bf16", 3), (32000, "bf16", 7),
+    (4096, "bf16", 1), (12296, "bf16", 2), (40000, "f32", 5),
+])
+def test_tilings(V, dtype, vpt, gpu):
+    log(f"tiling V={V} {dtype} vpt={vpt}")
+    traj, turn, mask, zs, zt = make_batch(V + vpt, V=V, dtype=dtype)
+    out, ref, rows = run_both(traj, turn, mask, zs, zt, vpt=vpt)
+    check_all(out, ref, mask, 1.0, rows)
+
+
+@pytest.mark.parametrize("V,dtype", [(1, "bf16"), (7, "f32"), (24, "bf16"), (1001, "bf16"),
+                                     (1003, "f32"), (50257, "bf16"), (8200, "f32")])
+def test_ragged_vocabularies(V, dtype, gpu):
+    """Vocabularies that are not a multiple of the 16-byte vector take the
+    scalar path; tiny ones leave most lanes of a chunk idle."""
+    log(f"ragged V={V} {dtype}")
+    traj, turn, mask, zs, zt = make_batch(V, V=V, dtype=dtype, n_traj=3)
+    out, ref, rows = run_both(traj, turn, mask, zs, zt)
+    check_all(out, ref, mask, 1.0, rows)
+
+
+@pytest.mark.parametrize("V,ld,dtype", [(2048, 2056, "bf16"), (2048, 2051, "bf16"),
+                                        (1000, 1004, "f32"), (1000, 1001, "f32")])
+def test_padded_row_stride(V, ld, dtype, gpu):
+    log(f"ld V={V} ld={ld} {dtype}")
+    traj, turn, mask, zs, zt = make_batch(ld, V=V, dtype=dtype)
+    out, ref, rows = run_both(traj, turn, mask, zs, zt, ld=ld)
+    check_all(out, ref, mask, 1.0, rows)
+    assert torch.isfinite(out[0]).all()
+
+
+# ----------------------------------------------------------------------------
+# options
+
+
+@pytest.mark.parametrize("grad_scale", [-2.5, 0.0, 1e-3])
+def test_grad_scale(grad_scale, gpu):
+    traj, turn, mask, zs, zt = make_batch(11)
+    out, ref, rows = run_both(traj, turn, mask, zs, zt, grad_scale=grad_scale)
+    if grad_scale == 0.0:
+        check_all(out[:1] + (None,) + out[2:], ref, mask, 1.0, rows)
+        assert torch.count_nonzero(out[1].float()).item() == 0
+    else:
+        check_all(out, ref, mask, grad_scale, rows)
+
+
+def test_forward_only(gpu):
+    traj, turn, mask, zs, zt = make_batch(12)
+    out, ref, rows = run_both(traj, turn, mask, zs, zt, grad=None)
+    assert out[1] is None
+    check_all(out, ref, mask, 1.0, rows)
+
+
+def test_in_place_equals_out_of_place_bitwise(gpu):
+    traj, turn, mask, zs_h, zt_h = make_batch(13, V=32000)
+    zs = to_device_logits(zs_h)
+    zt = to_device_logits(zt_h)
+    turn_d, traj_d, mask_d = ids_to_device(traj, turn, mask)
+    l1, g1, _, k1, _ = T.fwd_bwd(zs, zt, turn_d, traj_d, mask_d, 0.3, max_turns=8, token_kl=True)
+    zs2 = zs.clone()
+    l2, g2, _, k2, _ = T.fwd_bwd(zs2, zt, turn_d, traj_d, mask_d, 0.3, max_turns=8, grad="inplace",
+                                 token_kl=True)
+    torch.cuda.synchronize()
+    assert g2.data_ptr() == zs2.data_ptr()
+    assert torch.equal(g1.view(torch.int16), zs2.view(torch.int16))
+    assert torch.equal(l1, l2) and torch.equal(k1, k2)
+
+
+def test_runs_are_bitwise_deterministic(gpu):
+    traj, turn, mask, zs_h, zt_h = make_batch(14, V=151936 // 4, n_traj=6)
+    zs, zt = to_device_logits(zs_h), to_device_logits(zt_h)
+    turn_d, traj_d, mask_d = ids_to_device(traj, turn, mask)
+    outs = []
+    for _ in range(3):
+        st = T.new_turn_stats(8)
+        T.set_row_tiling(2)  # several chunks per row: exercises the exchange
+        try:
+            l, g, _, k, _ = T.fwd_bwd(zs, zt, turn_d, traj_d, mask_d, 0.6, max_turns=8,
+                                      turn_stats=st, token_kl=True)
+        finally:
+            T.set_row_tiling(0)
+        outs.append((l, g, st, k))
+    torch.cuda.synchronize()
+    for l, g, st, k in outs[1:]:
+        assert torch.equal(l, outs[0][0]) and torch.equal(k, outs[0][3])
+        assert torch.equal(g.view(torch.int16), outs[0][1].view(torch.int16))
+        assert torch.equal(st, outs[0][2])
+
+
+def test_accumulated_stats_equal_pooled_oracle(gpu):
+    """Three micro-batches accumulated on the device equal the oracle's
+    statistics recomputed from the pooled tokens (no merge formula)."""
+    stats = T.new_turn_stats(8)
+    parts = []
+    for k in range(3):
+        traj, turn, mask, zs_h, zt_h = make_batch(20 + k, V=3000)
+        zs, zt = to_device_logits(zs_h), to_device_logits(zt_h)
+        turn_d, traj_d, mask_d = ids_to_device(traj, turn, mask)
+        T.fwd_bwd(zs, zt, turn_d, traj_d, mask_d, 0.5, grad=None, max_turns=8, turn_stats=stats,
+                  accumulate_stats=k > 0)
+        ref = O.fwd_bwd(traj, turn, mask, 0.5, 8, lambda r: (zs_h[r], zt_h[r]), O.DTYPE_BF16)
+        parts.append((ref.seg, mask, ref.kl, ref.w))
+    torch.cuda.synchronize()
+    check_stats(stats, O.turn_stats(parts, 8))
+
+
+def test_loss_is_affine_in_alpha_and_mass_sums_to_loss(gpu):
+    traj, turn, mask, zs_h, zt_h = make_batch(30, V=5000)
+    zs, zt = to_device_logits(zs_h), to_device_logits(zt_h)
+    turn_d, traj_d, mask_d = ids_to_device(traj, turn, mask)
+    res = {}
+    for a in (0.0, 0.35, 1.0):
+        st = T.new_turn_stats(8)
+        l, _, _, _, _ = T.fwd_bwd(zs, zt, turn_d, traj_d, mask_d, a, grad=None, max_turns=8,
+                                  turn_stats=st)
+        res[a] = (l.cpu().numpy().astype(np.float64), T.read_turn_stats(st))
+    for a, (l, st) in res.items():
+        assert abs(l[0] - ((1 - a) * l[1] + a * l[2])) <= 1e-6 * abs(l[0])
+        assert abs(st["loss_mass"].sum() - l[0]) <= 1e-6 * abs(l[0])
+        assert np.allclose(l[1:], res[0.0][0][1:], rtol=0, atol=0)
+    assert abs(res[0.0][0][0] - res[0.0][0][1]) <= 1e-7 * res[0.0][0][1]
+    assert abs(res[1.0][0][0] - res[1.0][0][2]) <= 1e-7 * res[1.0][0][2]
+
+
+# ----------------------------------------------------------------------------
+# degenerate batches
+
+
+def test_identical_logits_give_exact_zeros(gpu):
+    traj, turn, mask, zs_h, _ = make_batch(40, V=32000)
+    zs = to_device_logits(zs_h)
+    turn_d, traj_d, mask_d = ids_to_device(traj, turn, mask)
+    for vpt in (0, 2):
+        T.set_row_tiling(vpt)
+        try:
+            l, g, _, k, _ = T.fwd_bwd(zs, zs, turn_d, traj_d, mask_d, 0.5, max_turns=8,
+                                      token_kl=True)
+        finally:
+            T.set_row_tiling(0)
+        torch.cuda.synchronize()
+        assert torch.count_nonzero(l).item() == 0
+        assert torch.count_nonzero(k).item() == 0
+        assert torch.count_nonzero(g.float()).item() == 0
+
+
+def test_empty_batch(gpu):
+    e = torch.empty((0, 128), dtype=torch.bfloat16, device=gpu)
+    i = torch.empty(0, dtype=torch.int32, device=gpu)
+    m = torch.empty(0, dtype=torch.uint8, device=gpu)
+    st = T.new_turn_stats(4)
+    st.fill_(7)
+    l, g, _, _, _ = T.fwd_bwd(e, e.clone(), i, i.clone(), m, 0.5, max_turns=4, turn_stats=st,
+                              accumulate_stats=True)
+    torch.cuda.synchronize()
+    assert torch.count_nonzero(l).item() == 0
+    assert torch.all(st == 7)  # accumulating an empty batch changes nothing
+    l, g, _, _, _ = T.fwd_bwd(e, e.clone(), i, i.clone(), m, 0.5, max_turns=4, turn_stats=st)
+    torch.cuda.synchronize()
+    assert torch.count_nonzero(st).item() == 0
+
+
+def test_fully_masked_batch(gpu):
+    traj, turn, mask, zs, zt = make_batch(41)
+    mask[:] = 0
+    out, ref, rows = run_both(traj, turn, mask, zs, zt)
+    assert ref.loss == (0.0, 0.0, 0.0)
+    check_all(out, ref, mask, 1.0, rows)
+    assert torch.count_nonzero(out[1].float()).item() == 0
+
+
+def test_single_giant_segment_and_one_token_segments(gpu):
+    rng = np.random.default_rng(42)
+    V = 512
+    # one trajectory, one turn of 3000 tokens
+    n = 3000
+    traj = np.zeros(n, np.int32)
+    turn = np.zeros(n, np.int32)
+    mask = (rng.uniform(size=n) < 0.7).astype(np.uint8)
+    zs = bf16_bits(rng.normal(0, 3, (n, V)))
+    zt = bf16_bits(rng.normal(0, 3, (n, V)))
+    out, ref, rows = run_both(traj, turn, mask, zs, zt, grad_rows=list(range(0, n, 97)))
+    check_all(out, ref, mask, 1.0, rows)
+    # 1-token segments: every token its own (trajectory, turn)
+    n = 2500
+    traj = (np.arange(n) // 50).astype(np.int32)
+    turn = (np.arange(n) % 50).astype(np.int32)
+    mask = (rng.uniform(size=n) < 0.5).astype(np.uint8)
+    zs = bf16_bits(rng.normal(0, 3, (n, V)))
+    zt = bf16_bits(rng.normal(0, 3, (n, V)))
+    out, ref, rows = run_both(traj, turn, mask, zs, zt, max_turns=50,
+                              grad_rows=list(range(0, n, 89)))
+    check_all(out, ref, mask, 1.0, rows)
+
+
+def test_extreme_but_finite_logits(gpu):
+    traj, turn, mask, zs, zt = make_batch(43, V=2048, dtype="f32", sigma=20.0, noise=5.0)
+    zs[::3] -= 1e4
+    zt[1::3] += 80.0
+    out, ref, rows = run_both(traj, turn, mask, zs, zt)
+    check_all(out, ref, mask, 1.0, rows)
+
+
+# ----------------------------------------------------------------------------
+# data errors detected on the device
+
+
+@pytest.mark.parametrize("case", ["pad_mask", "turn_high", "turn_negative", "traj_down",
+                                  "turn_down", "split_turn", "first_error_wins"])
+def test_device_errors_match_oracle(case, gpu):
+    traj, turn, mask, zs, zt = make_batch(50, pad=False, min_len=3)
+    traj, turn, mask = traj.copy(), turn.copy(), mask.copy()
+    n = len(traj)
+    i = n // 2
+    if case == "pad_mask":
+        traj[i] = -1
+        mask[i] = 1
+    elif case == "turn_high":
+        turn[i] = 8
+    elif case == "turn_negative":
+        turn[i] = -3
+    elif case == "traj_down":
+        traj[i:] = np.where(traj[i:] >= 0, traj[i:] - 100, traj[i:])
+    elif case == "turn_down":  # a later turn of a trajectory with a smaller id
+        seg = O.segments(traj, turn, mask, 8)
+        s_ = next(k for k in range(1, seg.count)
+                  if seg.traj[k] == seg.traj[k - 1] and seg.turn[k - 1] >= 1)
+        lo, hi = seg.start[s_], seg.start[s_] + seg.length[s_]
+        turn[lo:hi] = seg.turn[s_ - 1] - 1
+    elif case == "split_turn":  # padding inside a turn makes two runs of one turn id
+        seg = O.segments(traj, turn, mask, 8)
+        s_ = next(k for k in range(seg.count) if seg.length[k] >= 3)
+        j = seg.start[s_] + 1
+        traj[j] = -1
+        mask[j] = 0
+    elif case == "first_error_wins":
+        turn[i + 2] = 99
+        traj[i] = -1
+        mask[i] = 1
+    ref = O.segments(traj, turn, mask, 8)
+    assert ref.status != O.OK
+    zs_d, zt_d = to_device_logits(zs), to_device_logits(zt)
+    turn_d, traj_d, mask_d = ids_to_device(traj, turn, mask)
+    with pytest.raises(T.TurnKLError) as ei:
+        T.fwd_bwd(zs_d, zt_d, turn_d, traj_d, mask_d, 0.5, max_turns=8)
+    assert ei.value.code == ref.status, (case, ei.value.code, ref.status)
+    loss, _, _, _, ws = T.fwd_bwd(zs_d, zt_d, turn_d, traj_d, mask_d, 0.5, max_turns=8,
+                                  check=False)
+    assert ws.status() == ref.status
+    assert torch.isnan(loss).all()

@@ -1,0 +1,101 @@
+"""Parity of the HIP path with the CPU oracle on the five seeded workloads.
+
+The two small workloads are generated on the host and compared everywhere
+(every row's KL, every gradient row of the tiny batch, sampled gradient rows
+of the 4k-token batch).  The three vocabulary-151,936 workloads are generated
+in HBM at full size and run with the launch configuration bench.py times; the
+oracle reads every supervised row (copied from the generator's output before
+the call) for the loss, the per-token KL and the per-turn statistics, and
+sampled rows for the gradient.
+"""
+import numpy as np
+import pytest
+import torch
+
+import synth
+from gpu_support import (check_grad_rows, check_loss, check_segments, check_stats,
+                         check_token_kl, device_row_source, ids_to_device, log, oracle_dtype,
+                         sample_rows, to_device_logits)
+from oracle import turnkl_oracle as O
+from paper_2607_05804_amd import turnkl as T
+
+pytestmark = pytest.mark.gpu
+
+
+def _run(zs, zt, w, alpha, grad_scale, grad="new", ws=None):
+    turn, traj, mask = ids_to_device(w.traj_id, w.turn_id, w.loss_mask)
+    stats = T.new_turn_stats(w.max_turns)
+    loss, g, _, kl, ws = T.fwd_bwd(zs, zt, turn, traj, mask, alpha, grad_scale=grad_scale,
+                                   grad=grad, max_turns=w.max_turns, turn_stats=stats,
+                                   token_kl=True, workspace=ws)
+    torch.cuda.synchronize()
+    return loss, g, stats, kl, ws
+
+
+@pytest.mark.parametrize("name,grad_scale", [("tiny", 1.0), ("agent", 0.5)])
+def test_small_workloads(name, grad_scale, gpu):
+    w = synth.make(name)
+    alpha = w.alphas[0]
+    log(f"parity {name}: N={w.n_tokens} V={w.vocab} {w.dtype} alpha={alpha}")
+    zs_h, zt_h = w.host_logits(0, w.n_tokens)
+    zs, zt = to_device_logits(zs_h), to_device_logits(zt_h)
+    loss, g, stats, kl, ws = _run(zs, zt, w, alpha, grad_scale)
+    rows = list(range(w.n_tokens)) if name == "tiny" else sample_rows(w.loss_mask, 48, 8)
+    ref = O.fwd_bwd(w.traj_id, w.turn_id, w.loss_mask, alpha, w.max_turns,
+                    lambda r: (zs_h[r], zt_h[r]), oracle_dtype(zs.dtype), grad_scale, rows)
+    check_segments(ws, ref.seg)
+    check_loss(loss, ref.loss)
+    check_token_kl(kl, ref.kl, w.loss_mask)
+    check_stats(stats, ref.stats)
+    worst = check_grad_rows(g, ref, grad_scale, rows, w.loss_mask)
+    log(f"  loss gpu={loss.tolist()} ref={ref.loss} worst unweighted grad err={worst:.2e}")
+    # every unsupervised row of the gradient is zero
+    uns = np.nonzero(w.loss_mask == 0)[0]
+    if uns.size:
+        assert torch.count_nonzero(g[torch.from_numpy(uns).to(gpu)]).item() == 0
+
+
+def _full_size(name, gpu, check_alphas=None):
+    w = synth.make(name)
+    log(f"parity {name}: N={w.n_tokens} V={w.vocab} sup={w.n_supervised} in_place={w.in_place}")
+    zs, zt = w.device_logits()
+    rows = sample_rows(w.loss_mask, 24, 4, seed=1)
+    alphas = check_alphas or w.alphas
+    # oracle first: an in-place call overwrites the student logits
+    ref = O.fwd_bwd(w.traj_id, w.turn_id, w.loss_mask, alphas[0], w.max_turns,
+                    device_row_source(zs, zt), oracle_dtype(zs.dtype), 1.0, rows)
+    log(f"  oracle done: loss={ref.loss}")
+    assert ref.status == O.OK
+    ws = None
+    for k, alpha in enumerate(alphas):
+        last = k == len(alphas) - 1
+        grad = "inplace" if (w.in_place and last) else "new"
+        loss, g, stats, kl, ws = _run(zs, zt, w, alpha, 1.0, grad=grad, ws=ws)
+        w_a = O.token_weights(ref.seg, w.n_tokens, w.loss_mask, alpha)
+        w0 = O.token_weights(ref.seg, w.n_tokens, w.loss_mask, 0.0)
+        w1 = O.token_weights(ref.seg, w.n_tokens, w.loss_mask, 1.0)
+        ref_loss = O.losses(w_a, w0, w1, ref.kl)
+        ref_stats = O.turn_stats([(ref.seg, w.loss_mask, ref.kl, w_a)], w.max_turns)
+        check_segments(ws, ref.seg)
+        check_loss(loss, ref_loss)
+        check_token_kl(kl, ref.kl, w.loss_mask)
+        check_stats(stats, ref_stats)
+        ref_a = O.Result(O.OK, ref.seg, w_a, ref.kl, ref_loss, ref_stats,
+                         {r: (v[0], w_a[r] * v[0]) for r, v in ref.grads.items()})
+        worst = check_grad_rows(g, ref_a, 1.0, rows, w.loss_mask)
+        log(f"  alpha={alpha}: loss gpu={loss.tolist()} ref={ref_loss} worst grad err={worst:.2e}")
+        del g
+    del zs, zt
+    torch.cuda.empty_cache()
+
+
+def test_peaked_full_size_alpha_sweep(gpu):
+    _full_size("peaked", gpu)
+
+
+def test_long_horizon_full_size(gpu):
+    _full_size("long_horizon", gpu)
+
+
+def test_stress_full_size_in_place(gpu):
+    _full_size("stress", gpu)
