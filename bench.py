@@ -71,13 +71,37 @@ def cpu_baseline(w, sample_tokens: int):
                       f"vocabulary {w.vocab}), {dt:.1f} s"}
 
 
+def copy_probe(gib: float, steps: int) -> int:
+    """torch's device-to-device copy of a buffer of known size."""
+    import torch
+    n = int(gib * (1 << 30))
+    src = torch.empty(n, dtype=torch.uint8, device="cuda")
+    src.fill_(1)
+    dst = torch.empty_like(src)
+    dst.copy_(src)
+    torch.cuda.synchronize()
+    a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    a.record()
+    for _ in range(steps):
+        dst.copy_(src)
+    b.record()
+    torch.cuda.synchronize()
+    ms = a.elapsed_time(b) / steps
+    print(json.dumps({"copy_bytes": n, "read_plus_write_bytes": 2 * n, "ms": ms,
+                      "gbs": 2 * n / (ms * 1e-3) / 1e9}), flush=True)
+    return 0
+
+
 def main() -> int:
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=3)
-    ap.add_argument("--cpu-sample-tokens", type=int, default=4096)
+    ap.add_argument("--cpu-sample-tokens", type=int, default=16384)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--copy-probe", type=float, default=0.0, metavar="GIB",
+                    help="instead of the step, time a plain device copy of this many GiB "
+                         "(bandwidth context and counter calibration)")
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py runs on one GPU only (asked for --gpus {args.gpus}); the multi-GPU "
@@ -86,6 +110,9 @@ def main() -> int:
 
     import numpy as np
     import torch
+
+    if args.copy_probe > 0:
+        return copy_probe(args.copy_probe, args.steps)
 
     import synth
     from paper_2607_05804_amd import turnkl as T

@@ -120,7 +120,9 @@ size_t turnkl_workspace_bytes(int64_t n_tokens, int64_t vocab, int dtype, int32_
  *                                  NULL.  accumulate_stats != 0 merges this
  *                                  batch into the existing contents (counts and
  *                                  loss mass add; means and m2 merge exactly as
- *                                  if the tokens had been pooled); 0 overwrites.
+ *                                  if the tokens had been pooled; turns without
+ *                                  supervised tokens in this batch are left as
+ *                                  they are); 0 overwrites.
  * token_kl_out                     [n_tokens] float per-token KL (0 for
  *                                  unsupervised tokens), or NULL.
  * workspace, workspace_bytes       scratch of at least turnkl_workspace_bytes().

@@ -275,7 +275,7 @@ class Result:
     kl: np.ndarray           # per-token KL (float64; 0 where unsupervised)
     loss: tuple              # (L_blend, L_traj, L_turn)
     stats: np.ndarray        # STAT_DTYPE [max_turns]
-    grads: dict              # row -> (g_row unweighted float64 [V], G_row weighted)
+    grads: dict              # row -> unweighted dKL/dz_s float64 [V]; G = grad_scale * w[row] * g
 
 
 def fwd_bwd(traj_id, turn_id, loss_mask, alpha: float, max_turns: int, row_source,
@@ -310,6 +310,6 @@ def fwd_bwd(traj_id, turn_id, loss_mask, alpha: float, max_turns: int, row_sourc
         zs, zt = row_source(rows)
         _, g = row_kl(zs, zt, dtype, want_grad=True, n_threads=n_threads)
         for k, r in enumerate(rows.tolist()):
-            grads[r] = (g[k], grad_scale * w[r] * g[k])
+            grads[r] = g[k]
     stats = turn_stats([(seg, loss_mask, kl, w)], max_turns)
     return Result(OK, seg, w, kl, losses(w, w0, w1, kl), stats, grads)

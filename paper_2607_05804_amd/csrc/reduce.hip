@@ -58,7 +58,10 @@ __global__ __launch_bounds__(kMomThreads) void seg_moments(SegParams p, Ws ws, c
       out.lturn = sum / (b * t_b * (double)n);
       out.n = n;
     }
-    if (threadIdx.x == 0) ws.seg_stat[s] = out;
+    if (threadIdx.x == 0) {
+      ws.seg_stat[s] = out;
+      drain_stores();
+    }
   }
 }
 
@@ -136,16 +139,22 @@ __global__ __launch_bounds__(kFinThreads) void finalize(Ws ws, int max_turns, fl
   if (threadIdx.x != 0) return;
   Moments r = s_m[0];
   turnkl_turn_stat& o = stats[t];
+  if (accumulate && r.n == 0.0) return;  // nothing to merge at this turn
   if (accumulate) {
     const Moments old{(double)o.n_tokens, o.kl_mean, o.kl_m2, o.loss_mass, (long long)o.n_traj};
     r = merge(old, r);
   }
-  o.n_tokens = (long long)r.n;
-  o.n_traj = r.traj;
-  o.kl_mean = r.n > 0 ? r.mean : 0.0;
-  o.kl_m2 = r.n > 0 ? r.m2 : 0.0;
-  o.kl_var = r.n > 0 ? r.m2 / r.n : 0.0;
-  o.loss_mass = r.lm;
+  // one 64-bit store per field (no multi-dword store data to protect), then
+  // wait for them before the wave ends
+  volatile long long* oi = reinterpret_cast<volatile long long*>(&o);
+  volatile double* od = reinterpret_cast<volatile double*>(&o);
+  oi[0] = (long long)r.n;
+  oi[1] = r.traj;
+  od[2] = r.n > 0 ? r.mean : 0.0;
+  od[3] = r.n > 0 ? r.m2 : 0.0;
+  od[4] = r.n > 0 ? r.m2 / r.n : 0.0;
+  od[5] = r.lm;
+  drain_stores();
 }
 
 }  // namespace

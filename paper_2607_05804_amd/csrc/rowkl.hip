@@ -54,11 +54,25 @@ __device__ inline __amdgpu_buffer_rsrc_t chunk_rsrc(const void* base) {
   return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), 0, 0x7FFFFFFF, kRsrcWord3);
 }
 
+typedef unsigned u32x4 __attribute__((ext_vector_type(4)));
+typedef float f32x2 __attribute__((ext_vector_type(2)));
+typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
+
+// Store data must stay untouched for a while after a 16-byte store is
+// issued: on gfx950 the store can read its data registers later than the
+// compiler's wait states assume, so a register reused right after the store
+// (observed: the first data dword) lands in memory.  The row kernel pins each
+// store in program order and keeps its data live (keep_alive) across the next
+// pack's work, or across the end-of-task barrier for the last pack.
+__device__ inline void keep_alive(const u32x4& x) { asm volatile("" ::"v"(x)); }
+__device__ inline void keep_alive(unsigned x) { asm volatile("" ::"v"(x)); }
+
 template <bool kBf16, int kEpv>
 struct Pack;
 
 template <>
 struct Pack<true, 8> {  // 8 bf16 = 16 bytes
+  using Data = u32x4;
   unsigned w[4];
   __device__ void load(__amdgpu_buffer_rsrc_t r, int voff, int soff) {
     const auto u = __builtin_amdgcn_raw_buffer_load_b128(r, voff, soff, 0);
@@ -71,25 +85,26 @@ struct Pack<true, 8> {  // 8 bf16 = 16 bytes
     const unsigned x = w[j >> 1];
     return __uint_as_float((j & 1) ? (x & 0xFFFF0000u) : (x << 16));
   }
-  // flip = 0x80008000 negates both halves of every word
-  __device__ static void store(__amdgpu_buffer_rsrc_t r, int voff, int soff, const float (&g)[8],
-                               unsigned flip) {
-    __attribute__((ext_vector_type(4))) unsigned o;
+  // Round to bf16 (nearest even, v_cvt_pk_bf16_f32); flip = 0x80008000
+  // negates both halves of every word.
+  __device__ static Data encode(const float (&g)[8], unsigned flip) {
+    Data o;
 #pragma unroll
     for (int k = 0; k < 4; ++k) {
-      const __hip_bfloat162 h = __float22bfloat162_rn(make_float2(g[2 * k], g[2 * k + 1]));
-      o[k] = *reinterpret_cast<const unsigned*>(&h) ^ flip;
+      const f32x2 x = {g[2 * k], g[2 * k + 1]};
+      o[k] = __builtin_bit_cast(unsigned, __builtin_convertvector(x, bf16x2)) ^ flip;
     }
-    __builtin_amdgcn_raw_buffer_store_b128(o, r, voff, soff, 0);
+    return o;
   }
-  __device__ static void store_zero(__amdgpu_buffer_rsrc_t r, int voff, int soff) {
-    __attribute__((ext_vector_type(4))) unsigned o = {0u, 0u, 0u, 0u};
+  __device__ static Data zero() { return Data{0u, 0u, 0u, 0u}; }
+  __device__ static void store(__amdgpu_buffer_rsrc_t r, int voff, int soff, const Data& o) {
     __builtin_amdgcn_raw_buffer_store_b128(o, r, voff, soff, 0);
   }
 };
 
 template <>
 struct Pack<false, 4> {  // 4 fp32 = 16 bytes
+  using Data = u32x4;
   float f[4];
   __device__ void load(__amdgpu_buffer_rsrc_t r, int voff, int soff) {
     const auto u = __builtin_amdgcn_raw_buffer_load_b128(r, voff, soff, 0);
@@ -98,54 +113,53 @@ struct Pack<false, 4> {  // 4 fp32 = 16 bytes
   }
   __device__ void fence() { asm volatile("" : "+v"(f[0]), "+v"(f[1]), "+v"(f[2]), "+v"(f[3])); }
   __device__ float get(int j) const { return f[j]; }
-  __device__ static void store(__amdgpu_buffer_rsrc_t r, int voff, int soff, const float (&g)[4],
-                               unsigned flip) {
+  __device__ static Data encode(const float (&g)[4], unsigned flip) {
     const unsigned fl = flip << 16;  // sign bit of an fp32
-    __attribute__((ext_vector_type(4))) unsigned o;
+    Data o;
 #pragma unroll
     for (int k = 0; k < 4; ++k) o[k] = __float_as_uint(g[k]) ^ fl;
-    __builtin_amdgcn_raw_buffer_store_b128(o, r, voff, soff, 0);
+    return o;
   }
-  __device__ static void store_zero(__amdgpu_buffer_rsrc_t r, int voff, int soff) {
-    __attribute__((ext_vector_type(4))) unsigned o = {0u, 0u, 0u, 0u};
+  __device__ static Data zero() { return Data{0u, 0u, 0u, 0u}; }
+  __device__ static void store(__amdgpu_buffer_rsrc_t r, int voff, int soff, const Data& o) {
     __builtin_amdgcn_raw_buffer_store_b128(o, r, voff, soff, 0);
   }
 };
 
 template <>
 struct Pack<true, 1> {  // one bf16
+  using Data = unsigned;
   unsigned w;
   __device__ void load(__amdgpu_buffer_rsrc_t r, int voff, int soff) {
     w = __builtin_amdgcn_raw_buffer_load_b16(r, voff, soff, 0);
   }
   __device__ void fence() { asm volatile("" : "+v"(w)); }
   __device__ float get(int) const { return __uint_as_float(w << 16); }
-  __device__ static void store(__amdgpu_buffer_rsrc_t r, int voff, int soff, const float (&g)[1],
-                               unsigned flip) {
-    const __hip_bfloat16 h = __float2bfloat16(g[0]);
-    const unsigned short bits =
-        (unsigned short)(*reinterpret_cast<const unsigned short*>(&h) ^ (flip & 0xFFFFu));
-    __builtin_amdgcn_raw_buffer_store_b16(bits, r, voff, soff, 0);
+  __device__ static Data encode(const float (&g)[1], unsigned flip) {
+    const f32x2 x = {g[0], 0.0f};
+    return (__builtin_bit_cast(unsigned, __builtin_convertvector(x, bf16x2)) ^ flip) & 0xFFFFu;
   }
-  __device__ static void store_zero(__amdgpu_buffer_rsrc_t r, int voff, int soff) {
-    __builtin_amdgcn_raw_buffer_store_b16((unsigned short)0, r, voff, soff, 0);
+  __device__ static Data zero() { return 0u; }
+  __device__ static void store(__amdgpu_buffer_rsrc_t r, int voff, int soff, const Data& o) {
+    __builtin_amdgcn_raw_buffer_store_b16((unsigned short)o, r, voff, soff, 0);
   }
 };
 
 template <>
 struct Pack<false, 1> {  // one fp32
+  using Data = unsigned;
   float f;
   __device__ void load(__amdgpu_buffer_rsrc_t r, int voff, int soff) {
     f = __uint_as_float(__builtin_amdgcn_raw_buffer_load_b32(r, voff, soff, 0));
   }
   __device__ void fence() { asm volatile("" : "+v"(f)); }
   __device__ float get(int) const { return f; }
-  __device__ static void store(__amdgpu_buffer_rsrc_t r, int voff, int soff, const float (&g)[1],
-                               unsigned flip) {
-    __builtin_amdgcn_raw_buffer_store_b32(__float_as_uint(g[0]) ^ (flip << 16), r, voff, soff, 0);
+  __device__ static Data encode(const float (&g)[1], unsigned flip) {
+    return __float_as_uint(g[0]) ^ (flip << 16);
   }
-  __device__ static void store_zero(__amdgpu_buffer_rsrc_t r, int voff, int soff) {
-    __builtin_amdgcn_raw_buffer_store_b32(0u, r, voff, soff, 0);
+  __device__ static Data zero() { return 0u; }
+  __device__ static void store(__amdgpu_buffer_rsrc_t r, int voff, int soff, const Data& o) {
+    __builtin_amdgcn_raw_buffer_store_b32(o, r, voff, soff, 0);
   }
 };
 
@@ -179,6 +193,9 @@ __global__ __launch_bounds__(kRowThreads) void rowkl_kernel(RowParams p) {
   const int wid = tid / kWave;
   const unsigned n_tasks = (unsigned)(p.n_rows * p.n_chunks);
   const long long n_packs = p.vocab / kEpv;
+  // data of this wave's most recent 16-byte store, kept live until the next
+  // task's loads are issued (see keep_alive)
+  typename P::Data carry = P::zero();
 
   for (;;) {
     if (tid == 0) {
@@ -187,7 +204,7 @@ __global__ __launch_bounds__(kRowThreads) void rowkl_kernel(RowParams p) {
     }
     __syncthreads();
     const unsigned task = __builtin_amdgcn_readfirstlane(s_task);  // uniform: keep it scalar
-    if (task >= n_tasks) return;
+    if (task >= n_tasks) break;
     const long long row = (long long)(task / (unsigned)p.n_chunks);
     const int c = (int)(task - (unsigned)row * (unsigned)p.n_chunks);
     const long long pack_lo = n_packs * c / p.n_chunks;
@@ -202,10 +219,14 @@ __global__ __launch_bounds__(kRowThreads) void rowkl_kernel(RowParams p) {
 
     if (!p.mask[row]) {
       if (p.grad) {
+        const typename P::Data z = P::zero();
         const auto rg = chunk_rsrc(static_cast<char*>(p.grad) + (row * p.ld_g + pack_lo * kEpv) * kEs);
 #pragma unroll
         for (int v = 0; v < kVpt; ++v)
-          if (valid[v]) P::store_zero(rg, lane_off, v * kStep);
+          if (valid[v]) P::store(rg, lane_off, v * kStep, z);
+        __builtin_amdgcn_sched_barrier(0);
+        keep_alive(carry);
+        carry = z;
       }
       __syncthreads();
       continue;
@@ -224,81 +245,117 @@ __global__ __launch_bounds__(kRowThreads) void rowkl_kernel(RowParams p) {
       xs[v].load(rs, vo, so);
       xt[v].load(rt, vo, so);
     }
+    __builtin_amdgcn_sched_barrier(0);
+    keep_alive(carry);  // the previous task's last store has long read its data
 
-    // ---- chunk maxima
+    // ---- chunk partials.  Any reference value m works for the sums
+    // S = sum 2^(a log2e - m log2e) as long as no term overflows, so the
+    // reference is the maximum over each thread's first pack only; in the rare
+    // case that a logit exceeds it by ~88 a sum overflows and the chunk is
+    // redone against its exact maximum.  (The row merge below accounts for
+    // whatever reference each chunk used.)
+    // ---- chunk partials.  Any reference m works for S = sum 2^(a log2e - m log2e)
+    // as long as no term overflows, so the reference is the maximum over each
+    // thread's first pack only.  If a logit exceeds it by ~88 a sum overflows
+    // (rare; uniform across the block) and the chunk is redone against its
+    // exact maximum.  The row merge accounts for whichever reference was used.
+#define TURNKL_BLOCK_MAX2(MS, MT)                        \
+  {                                                      \
+    MS = wave_max(MS);                                   \
+    MT = wave_max(MT);                                   \
+    if (lane == 0) {                                     \
+      s_max[0][wid] = MS;                                \
+      s_max[1][wid] = MT;                                \
+    }                                                    \
+    __syncthreads();                                     \
+    MS = s_max[0][0];                                    \
+    MT = s_max[1][0];                                    \
+    _Pragma("unroll") for (int w = 1; w < kRowWaves; ++w) { \
+      MS = fmaxf(MS, s_max[0][w]);                       \
+      MT = fmaxf(MT, s_max[1][w]);                       \
+    }                                                    \
+  }
+#define TURNKL_FENCE_ALL()                                \
+  _Pragma("unroll") for (int v = 0; v < kVpt; ++v) {     \
+    xs[v].fence();                                       \
+    xt[v].fence();                                       \
+  }
+#define TURNKL_CHUNK_SUMS(M2S, M2T, SS, AA, ST)                               \
+  {                                                                           \
+    SS = 0.0f;                                                                \
+    AA = 0.0f;                                                                \
+    ST = 0.0f;                                                                \
+    _Pragma("unroll") for (int v = 0; v < kVpt; ++v) {                        \
+      _Pragma("unroll") for (int j = 0; j < kEpv; ++j) {                      \
+        const float a = xs[v].get(j);                                         \
+        const float b = xt[v].get(j);                                         \
+        float es = exp2_fast(fmaf(a, kLog2e, -(M2S)));                        \
+        float et = exp2_fast(fmaf(b, kLog2e, -(M2T)));                        \
+        float d = a - b;                                                      \
+        if (kCheckAll || v == kVpt - 1) {                                     \
+          es = valid[v] ? es : 0.0f;                                          \
+          et = valid[v] ? et : 0.0f;                                          \
+          d = valid[v] ? d : 0.0f;                                            \
+        }                                                                     \
+        SS += es;                                                             \
+        AA = fmaf(es, d, AA);                                                 \
+        ST += et;                                                             \
+      }                                                                       \
+    }                                                                         \
+    SS = wave_sum(SS);                                                        \
+    AA = wave_sum(AA);                                                        \
+    ST = wave_sum(ST);                                                        \
+    if (lane == 0) {                                                          \
+      s_sum[0][wid] = SS;                                                     \
+      s_sum[1][wid] = AA;                                                     \
+      s_sum[2][wid] = ST;                                                     \
+    }                                                                         \
+    __syncthreads();                                                          \
+    SS = s_sum[0][0];                                                         \
+    AA = s_sum[1][0];                                                         \
+    ST = s_sum[2][0];                                                         \
+    _Pragma("unroll") for (int w = 1; w < kRowWaves; ++w) {                   \
+      SS += s_sum[0][w];                                                      \
+      AA += s_sum[1][w];                                                      \
+      ST += s_sum[2][w];                                                      \
+    }                                                                         \
+  }
+
     float ms = -INFINITY, mt = -INFINITY;
 #pragma unroll
-    for (int v = 0; v < kVpt; ++v) {
-#pragma unroll
-      for (int j = 0; j < kEpv; ++j) {
-        const float a = xs[v].get(j);
-        const float b = xt[v].get(j);
-        ms = fmaxf(ms, valid[v] ? a : -INFINITY);
-        mt = fmaxf(mt, valid[v] ? b : -INFINITY);
-      }
+    for (int j = 0; j < kEpv; ++j) {
+      ms = fmaxf(ms, valid[0] ? xs[0].get(j) : -INFINITY);
+      mt = fmaxf(mt, valid[0] ? xt[0].get(j) : -INFINITY);
     }
-    ms = wave_max(ms);
-    mt = wave_max(mt);
-    if (lane == 0) {
-      s_max[0][wid] = ms;
-      s_max[1][wid] = mt;
-    }
-    __syncthreads();
-    ms = s_max[0][0];
-    mt = s_max[1][0];
+    TURNKL_BLOCK_MAX2(ms, mt)
+    float m2s = ms * kLog2e;
+    float m2t = mt * kLog2e;
+    TURNKL_FENCE_ALL()
+    float ss, aa, st;
+    TURNKL_CHUNK_SUMS(m2s, m2t, ss, aa, st)
+    if (!(__builtin_isfinite(ss) && __builtin_isfinite(st))) {
+      __syncthreads();  // s_max / s_sum are about to be reused
+      TURNKL_FENCE_ALL()
+      ms = -INFINITY;
+      mt = -INFINITY;
 #pragma unroll
-    for (int w = 1; w < kRowWaves; ++w) {
-      ms = fmaxf(ms, s_max[0][w]);
-      mt = fmaxf(mt, s_max[1][w]);
-    }
-    const float m2s = ms * kLog2e;
-    const float m2t = mt * kLog2e;
+      for (int v = 0; v < kVpt; ++v) {
 #pragma unroll
-    for (int v = 0; v < kVpt; ++v) {
-      xs[v].fence();
-      xt[v].fence();
-    }
-
-    // ---- chunk sums
-    float ss = 0.0f, aa = 0.0f, st = 0.0f;
-#pragma unroll
-    for (int v = 0; v < kVpt; ++v) {
-#pragma unroll
-      for (int j = 0; j < kEpv; ++j) {
-        const float a = xs[v].get(j);
-        const float b = xt[v].get(j);
-        float es = exp2_fast(fmaf(a, kLog2e, -m2s));
-        float et = exp2_fast(fmaf(b, kLog2e, -m2t));
-        float d = a - b;
-        if (kCheckAll || v == kVpt - 1) {
-          es = valid[v] ? es : 0.0f;
-          et = valid[v] ? et : 0.0f;
-          d = valid[v] ? d : 0.0f;
+        for (int j = 0; j < kEpv; ++j) {
+          ms = fmaxf(ms, valid[v] ? xs[v].get(j) : -INFINITY);
+          mt = fmaxf(mt, valid[v] ? xt[v].get(j) : -INFINITY);
         }
-        ss += es;
-        aa = fmaf(es, d, aa);
-        st += et;
       }
+      TURNKL_BLOCK_MAX2(ms, mt)
+      m2s = ms * kLog2e;
+      m2t = mt * kLog2e;
+      TURNKL_FENCE_ALL()
+      __syncthreads();
+      TURNKL_CHUNK_SUMS(m2s, m2t, ss, aa, st)
     }
-    ss = wave_sum(ss);
-    aa = wave_sum(aa);
-    st = wave_sum(st);
-    if (lane == 0) {
-      s_sum[0][wid] = ss;
-      s_sum[1][wid] = aa;
-      s_sum[2][wid] = st;
-    }
-    __syncthreads();
-    ss = s_sum[0][0];
-    aa = s_sum[1][0];
-    st = s_sum[2][0];
-#pragma unroll
-    for (int w = 1; w < kRowWaves; ++w) {
-      ss += s_sum[0][w];
-      aa += s_sum[1][w];
-      st += s_sum[2][w];
-    }
-
+#undef TURNKL_CHUNK_SUMS
+#undef TURNKL_FENCE_ALL
+#undef TURNKL_BLOCK_MAX2
 #pragma unroll
     for (int v = 0; v < kVpt; ++v) {
       xs[v].fence();
@@ -333,6 +390,7 @@ __global__ __launch_bounds__(kRowThreads) void rowkl_kernel(RowParams p) {
       __syncthreads();
       if (s_timeout) {
         if (tid == 0) atomicMin(&p.hdr->err_key, err_key(0, kPrioTimeout));
+        drain_stores();
         return;
       }
       rm2s = -INFINITY;
@@ -363,6 +421,7 @@ __global__ __launch_bounds__(kRowThreads) void rowkl_kernel(RowParams p) {
       const float shift = (rm2s + log2f(rss)) - log2f(fabsf(sc));
       const unsigned flip = sc < 0.0f ? 0x80008000u : 0u;
       const auto rg = chunk_rsrc(static_cast<char*>(p.grad) + (row * p.ld_g + pack_lo * kEpv) * kEs);
+      typename P::Data prev = P::zero();
 #pragma unroll
       for (int v = 0; v < kVpt; ++v) {
         float out[kEpv];
@@ -372,11 +431,19 @@ __global__ __launch_bounds__(kRowThreads) void rowkl_kernel(RowParams p) {
           const float b = xt[v].get(j);
           out[j] = exp2_fast(fmaf(a, kLog2e, -shift)) * ((a - b) - mu);
         }
-        if (valid[v]) P::store(rg, lane_off, v * kStep, out, flip);
+        const typename P::Data cur = P::encode(out, flip);
+        if (valid[v]) P::store(rg, lane_off, v * kStep, cur);
+        // keep the store here, so the next pack's work separates it from any
+        // reuse of its data registers; the previous pack's data is free now
+        __builtin_amdgcn_sched_barrier(0);
+        keep_alive(prev);
+        prev = cur;
       }
+      carry = prev;
     }
     __syncthreads();
   }
+  drain_stores();
 }
 
 // ---------------------------------------------------------------------------

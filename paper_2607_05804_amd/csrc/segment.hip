@@ -103,10 +103,12 @@ __global__ __launch_bounds__(kScanThreads) void seg_offsets(Ws ws, long long nbl
   if (threadIdx.x == 0) {
     unsigned long long e = kNoError;
     for (int w = 0; w < kScanThreads / kWave; ++w) e = s_err[w] < e ? s_err[w] : e;
-    ws.hdr->err_key = e;
-    ws.hdr->ticket = 0u;
-    ws.hdr->n_seg = carry;
-    ws.hdr->b_eff = 0;
+    volatile Header* h = ws.hdr;
+    h->err_key = e;
+    h->ticket = 0u;
+    h->n_seg = carry;
+    h->b_eff = 0;
+    drain_stores();
   }
 }
 
@@ -195,6 +197,7 @@ __global__ __launch_bounds__(kSegThreads) void token_weights(SegParams p, Ws ws,
     if (slot_words) {
       unsigned long long* sl = ws.slots + i * (long long)slot_words;
       for (int q = 0; q < slot_words; ++q) sl[q] = 0ull;
+      drain_stores();
     }
   }
 }

@@ -3,15 +3,17 @@ the CPU oracle on the same seeded inputs, and compare.
 
 Tolerances (derived in the design doc from the fp32 arithmetic of the kernels):
   * segment table, counts, survivors, status codes: bit-exact;
-  * loss (each of L_blend, L_traj, L_turn): relative 1e-4;
+  * loss (each of L_blend, L_traj, L_turn): relative 1e-4, with an absolute
+    floor of 1e-6 (each per-token KL carries ~1e-7 absolute error from the
+    fp32 exp2 / log2 of the row scalars, visible only when KL is ~0);
   * per-token KL: |d| <= 2e-4 |KL| + 5e-6;
   * gradient, compared unweighted (g_hat = G / (grad_scale * w_i)):
       |g_hat - g| <= 2e-2 absolute (the stated bar), and the tighter
       |g_hat - g| <= 2^-8 |g| + 2e-5 for bf16 output (about one bf16 ulp),
       |g_hat - g| <= 1e-4 |g| + 2e-6 for fp32 output;
     unsupervised rows must be exactly zero;
-  * per-turn stats: mean and loss mass relative 1e-4, variance
-    |d| <= 1e-4 var + 1e-8.
+  * per-turn stats: mean and loss mass relative 1e-4 (absolute floor 1e-6),
+    variance |d| <= 1e-4 var + 1e-8.
 """
 from __future__ import annotations
 
@@ -66,7 +68,7 @@ def check_segments(ws: T.Workspace, ref: O.Segments) -> None:
 def check_loss(loss: torch.Tensor, ref_loss, rtol=1e-4) -> None:
     got = loss.cpu().numpy().astype(np.float64)
     for g, r, name in zip(got, ref_loss, ("L_blend", "L_traj", "L_turn")):
-        assert abs(g - r) <= rtol * abs(r) + 1e-12, (name, g, r, abs(g - r) / max(abs(r), 1e-30))
+        assert abs(g - r) <= rtol * abs(r) + 1e-6, (name, g, r, abs(g - r) / max(abs(r), 1e-30))
 
 
 def check_token_kl(kl_dev: torch.Tensor, ref_kl: np.ndarray, mask: np.ndarray) -> None:
@@ -84,7 +86,7 @@ def check_stats(stats_buf: torch.Tensor, ref: np.ndarray) -> None:
     assert np.array_equal(got["n_traj"], ref["n_traj"])
     for f in ("kl_mean", "loss_mass"):
         err = np.abs(got[f] - ref[f])
-        assert np.all(err <= 1e-4 * np.abs(ref[f]) + 1e-12), (f, np.max(err))
+        assert np.all(err <= 1e-4 * np.abs(ref[f]) + 1e-6), (f, np.max(err))
     err = np.abs(got["kl_var"] - ref["kl_var"])
     assert np.all(err <= 1e-4 * ref["kl_var"] + 1e-8), ("kl_var", np.max(err))
     err = np.abs(got["kl_m2"] - ref["kl_m2"])
@@ -103,7 +105,7 @@ def check_grad_rows(grad_dev: torch.Tensor, ref: O.Result, grad_scale: float, ro
         if not mask[r]:
             assert np.all(G[k] == 0.0), ("unsupervised row not zero", r)
             continue
-        g_ref = ref.grads[r][0]
+        g_ref = ref.grads[r]
         scale = grad_scale * ref.w[r]
         g_hat = G[k] / scale
         err = np.abs(g_hat - g_ref)
