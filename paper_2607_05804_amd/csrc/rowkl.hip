@@ -34,6 +34,13 @@
 #include "block_ops.h"
 #include "turnkl_internal.h"
 
+// No implicit FMA contraction in this file: every fused multiply-add the
+// kernel wants is written as fmaf.  Contraction would evaluate the student
+// and teacher halves of a difference asymmetrically (x*c - y*c becoming
+// fma(x, c, -(y*c)) leaves the rounding error of y*c when x == y), so
+// identical logits would no longer give exactly zero KL and gradient.
+#pragma clang fp contract(off)
+
 namespace turnkl {
 namespace {
 
@@ -41,6 +48,10 @@ constexpr float kLog2e = 1.4426950408889634f;
 constexpr float kLn2 = 0.6931471805599453f;
 constexpr int kRowWaves = kRowThreads / kWave;
 constexpr int kSpinLimit = 1 << 22;
+// Reference magnitude (log2 units, i.e. logits times log2 e) above which a
+// chunk, and then its row, subtracts its references per element.  Below it
+// the fast path's error term, a few u |m_s - m_t|, stays under 1e-5.
+constexpr float kFar2 = 64.0f * kLog2e;
 
 // ---------------------------------------------------------------------------
 // packs of kEpv elements moved with one load/store
@@ -165,8 +176,52 @@ struct Pack<false, 1> {  // one fp32
 
 __device__ inline float exp2_fast(float x) { return __builtin_amdgcn_exp2f(x); }
 
-__device__ inline unsigned long long tagged(float v) {
-  return (1ull << 32) | (unsigned long long)__float_as_uint(v);
+// Exchange word: the tag in the high half marks it written and says how the
+// chunk's partials are expressed (kTagFast / kTagOffset); value in the low half.
+constexpr unsigned kTagFast = 1;
+constexpr unsigned kTagOffset = 2;
+__device__ inline unsigned long long tagged(float v, unsigned tag) {
+  return ((unsigned long long)tag << 32) | (unsigned long long)__float_as_uint(v);
+}
+
+// Row merge.  A chunk reports (M_s, S_s, A, M_t, S_t) in one of two forms:
+//  fast (tag kTagFast): M in log2 units (logits times log2 e),
+//    S_s = sum 2^(a log2e - M_s),  A = sum 2^(a log2e - M_s) (a - b),  S_t likewise;
+//  offset (kTagOffset): M in logit units,
+//    S_s = sum 2^((a - M_s) log2e),  A = sum 2^((a - M_s) log2e) ((a - M_s) - (b - M_t)).
+// The row works against natural references (R_s, R_t) >= every chunk's
+// reference and accumulates, in chunk order,
+//   S_s = sum_v 2^((a_v - R_s) log2e),  S_t likewise,
+//   A   = sum_v 2^((a_v - R_s) log2e) ((a_v - R_s) - (b_v - R_t)),
+// so no term carries the magnitude of the logits: KL = A / S_s + ln(S_t / S_s).
+// A fast chunk scales by 2^(M_s - R_s log2e) (one FMA for the exponent) and
+// its A becomes A - S_s (R_s - R_t), which costs an error of ~u |R_s - R_t|;
+// an offset chunk scales by 2^((M_s - R_s) log2e) and gains
+// S_s ((M_s - R_s) - (M_t - R_t)), both differences small.
+struct RowSums {
+  float ss, aa, st;
+};
+
+// natural reference of a chunk: a logit-unit value at or above its own
+__device__ inline float natural_ref(bool offset, float m) { return offset ? m : m * kLn2; }
+
+__device__ inline void merge_chunk(bool offset, float ms, float ss, float aa, float mt, float st,
+                                   float rs, float rt, float d_r, RowSums& r) {
+  float fs, ft;
+  if (offset) {
+    const float ds = ms - rs;
+    const float dt = mt - rt;
+    fs = exp2f(ds * kLog2e);
+    ft = exp2f(dt * kLog2e);
+    aa = fmaf(ss, ds - dt, aa);
+  } else {
+    fs = exp2f(fmaf(-rs, kLog2e, ms));
+    ft = exp2f(fmaf(-rt, kLog2e, mt));
+    aa = fmaf(-ss, d_r, aa);
+  }
+  r.ss = fmaf(ss, fs, r.ss);
+  r.aa = fmaf(aa, fs, r.aa);
+  r.st = fmaf(st, ft, r.st);
 }
 
 // One (row, chunk) task per iteration.  A chunk is the pack range
@@ -184,6 +239,8 @@ __global__ __launch_bounds__(kRowThreads) void rowkl_kernel(RowParams p) {
   __shared__ float s_max[2][kRowWaves];
   __shared__ float s_sum[3][kRowWaves];
   __shared__ float s_part[kMaxPartialWords];
+  __shared__ unsigned s_tag[kMaxChunks];
+  __shared__ int s_lo[kMaxChunks + 1];  // first pack of each chunk
   __shared__ unsigned s_task;
   __shared__ int s_timeout;
 
@@ -191,8 +248,10 @@ __global__ __launch_bounds__(kRowThreads) void rowkl_kernel(RowParams p) {
   const int tid = threadIdx.x;
   const int lane = tid & (kWave - 1);
   const int wid = tid / kWave;
-  const unsigned n_tasks = (unsigned)(p.n_rows * p.n_chunks);
-  const long long n_packs = p.vocab / kEpv;
+  const unsigned n_tasks = (unsigned)p.n_rows * (unsigned)p.n_chunks;
+  // balanced chunks: chunk c is packs [n_packs c / n_chunks, n_packs (c + 1) / n_chunks)
+  for (int k = tid; k <= p.n_chunks; k += kRowThreads)
+    s_lo[k] = (int)((long long)p.n_packs * k / p.n_chunks);
   // data of this wave's most recent 16-byte store, kept live until the next
   // task's loads are issued (see keep_alive)
   typename P::Data carry = P::zero();
@@ -207,9 +266,9 @@ __global__ __launch_bounds__(kRowThreads) void rowkl_kernel(RowParams p) {
     if (task >= n_tasks) break;
     const long long row = (long long)(task / (unsigned)p.n_chunks);
     const int c = (int)(task - (unsigned)row * (unsigned)p.n_chunks);
-    const long long pack_lo = n_packs * c / p.n_chunks;
-    const long long pack_hi = n_packs * (c + 1) / p.n_chunks;
-    const int n_valid = (int)(pack_hi - pack_lo);  // packs in this chunk
+    const int pack_lo = __builtin_amdgcn_readfirstlane(s_lo[c]);
+    const int n_valid = __builtin_amdgcn_readfirstlane(s_lo[c + 1]) - pack_lo;  // packs in this chunk
+    const long long col = (long long)pack_lo * kEpv;  // first element of the chunk
     const int lane_off = tid * kPackBytes;
 
     bool valid[kVpt];
@@ -220,13 +279,14 @@ __global__ __launch_bounds__(kRowThreads) void rowkl_kernel(RowParams p) {
     if (!p.mask[row]) {
       if (p.grad) {
         const typename P::Data z = P::zero();
-        const auto rg = chunk_rsrc(static_cast<char*>(p.grad) + (row * p.ld_g + pack_lo * kEpv) * kEs);
+        const auto rg = chunk_rsrc(static_cast<char*>(p.grad) + (row * p.ld_g + col) * kEs);
 #pragma unroll
         for (int v = 0; v < kVpt; ++v)
           if (valid[v]) P::store(rg, lane_off, v * kStep, z);
-        __builtin_amdgcn_sched_barrier(0);
+        // the zeros sit in registers the loop's phi copies may take over
+        // right away: let the stores complete first
+        drain_stores();
         keep_alive(carry);
-        carry = z;
       }
       __syncthreads();
       continue;
@@ -234,8 +294,8 @@ __global__ __launch_bounds__(kRowThreads) void rowkl_kernel(RowParams p) {
 
     // ---- load the chunk of both rows into registers (an out-of-chunk pack
     // reads the chunk's first pack instead and is masked below)
-    const auto rs = chunk_rsrc(static_cast<const char*>(p.zs) + (row * p.ld_s + pack_lo * kEpv) * kEs);
-    const auto rt = chunk_rsrc(static_cast<const char*>(p.zt) + (row * p.ld_t + pack_lo * kEpv) * kEs);
+    const auto rs = chunk_rsrc(static_cast<const char*>(p.zs) + (row * p.ld_s + col) * kEs);
+    const auto rt = chunk_rsrc(static_cast<const char*>(p.zt) + (row * p.ld_t + col) * kEs);
     P xs[kVpt], xt[kVpt];
 #pragma unroll
     for (int v = 0; v < kVpt; ++v) {
@@ -248,17 +308,14 @@ __global__ __launch_bounds__(kRowThreads) void rowkl_kernel(RowParams p) {
     __builtin_amdgcn_sched_barrier(0);
     keep_alive(carry);  // the previous task's last store has long read its data
 
-    // ---- chunk partials.  Any reference value m works for the sums
-    // S = sum 2^(a log2e - m log2e) as long as no term overflows, so the
-    // reference is the maximum over each thread's first pack only; in the rare
-    // case that a logit exceeds it by ~88 a sum overflows and the chunk is
-    // redone against its exact maximum.  (The row merge below accounts for
-    // whatever reference each chunk used.)
-    // ---- chunk partials.  Any reference m works for S = sum 2^(a log2e - m log2e)
-    // as long as no term overflows, so the reference is the maximum over each
-    // thread's first pack only.  If a logit exceeds it by ~88 a sum overflows
-    // (rare; uniform across the block) and the chunk is redone against its
-    // exact maximum.  The row merge accounts for whichever reference was used.
+    // ---- chunk partials.  Any reference works for S = sum 2^(a log2e - M)
+    // as long as no term overflows, so the fast path's reference is the
+    // maximum over each thread's first pack only, folded into one FMA per
+    // exponent (log2 units: the fast form of merge_chunk).  A chunk whose
+    // reference is far from zero (|max| > 64), or whose sums overflow, is
+    // redone against its exact maximum with the references subtracted per
+    // element, directly in natural-reference form (uniform branch; cold for
+    // ordinary logits).
 #define TURNKL_BLOCK_MAX2(MS, MT)                        \
   {                                                      \
     MS = wave_max(MS);                                   \
@@ -280,17 +337,27 @@ __global__ __launch_bounds__(kRowThreads) void rowkl_kernel(RowParams p) {
     xs[v].fence();                                       \
     xt[v].fence();                                       \
   }
-#define TURNKL_CHUNK_SUMS(M2S, M2T, SS, AA, ST)                               \
+  // OFFSET (a literal): subtract natural references RS, RT per element;
+  // otherwise RS, RT are log2-unit references folded into the exponent FMA
+#define TURNKL_CHUNK_SUMS(OFFSET, RS, RT, SS, AA, ST)                         \
   {                                                                           \
     SS = 0.0f;                                                                \
     AA = 0.0f;                                                                \
     ST = 0.0f;                                                                \
     _Pragma("unroll") for (int v = 0; v < kVpt; ++v) {                        \
       _Pragma("unroll") for (int j = 0; j < kEpv; ++j) {                      \
-        const float a = xs[v].get(j);                                         \
-        const float b = xt[v].get(j);                                         \
-        float es = exp2_fast(fmaf(a, kLog2e, -(M2S)));                        \
-        float et = exp2_fast(fmaf(b, kLog2e, -(M2T)));                        \
+        float a = xs[v].get(j);                                               \
+        float b = xt[v].get(j);                                               \
+        float es, et;                                                         \
+        if (OFFSET) {                                                         \
+          a -= (RS);                                                          \
+          b -= (RT);                                                          \
+          es = exp2_fast(a * kLog2e);                                         \
+          et = exp2_fast(b * kLog2e);                                         \
+        } else {                                                              \
+          es = exp2_fast(fmaf(a, kLog2e, -(RS)));                             \
+          et = exp2_fast(fmaf(b, kLog2e, -(RT)));                             \
+        }                                                                     \
         float d = a - b;                                                      \
         if (kCheckAll || v == kVpt - 1) {                                     \
           es = valid[v] ? es : 0.0f;                                          \
@@ -332,8 +399,10 @@ __global__ __launch_bounds__(kRowThreads) void rowkl_kernel(RowParams p) {
     float m2t = mt * kLog2e;
     TURNKL_FENCE_ALL()
     float ss, aa, st;
-    TURNKL_CHUNK_SUMS(m2s, m2t, ss, aa, st)
-    if (!(__builtin_isfinite(ss) && __builtin_isfinite(st))) {
+    TURNKL_CHUNK_SUMS(false, m2s, m2t, ss, aa, st)
+    const bool offset = !(fmaxf(fabsf(m2s), fabsf(m2t)) <= kFar2) ||
+                        !(__builtin_isfinite(ss) && __builtin_isfinite(st));
+    if (offset) {
       __syncthreads();  // s_max / s_sum are about to be reused
       TURNKL_FENCE_ALL()
       ms = -INFINITY;
@@ -347,11 +416,11 @@ __global__ __launch_bounds__(kRowThreads) void rowkl_kernel(RowParams p) {
         }
       }
       TURNKL_BLOCK_MAX2(ms, mt)
-      m2s = ms * kLog2e;
-      m2t = mt * kLog2e;
+      m2s = ms;  // from here on: natural references
+      m2t = mt;
       TURNKL_FENCE_ALL()
       __syncthreads();
-      TURNKL_CHUNK_SUMS(m2s, m2t, ss, aa, st)
+      TURNKL_CHUNK_SUMS(true, m2s, m2t, ss, aa, st)
     }
 #undef TURNKL_CHUNK_SUMS
 #undef TURNKL_FENCE_ALL
@@ -362,18 +431,25 @@ __global__ __launch_bounds__(kRowThreads) void rowkl_kernel(RowParams p) {
       xt[v].fence();
     }
 
-    // ---- row scalars: merge the chunks of the row in chunk order
-    float rm2s = m2s, rss = ss, raa = aa, rm2t = m2t, rst = st;
+    // ---- row scalars: publish this chunk's partials, read the row mates',
+    // merge all of them in chunk order against the row references (the
+    // largest chunk references; see merge_chunk), so every workgroup of the
+    // row computes the same bits.  If any chunk took the offset path, the
+    // whole row writes its gradient with offsets too.
+    RowSums r{0.0f, 0.0f, 0.0f};
+    float r_s, r_t;  // row references, logit units
+    bool row_offset = offset;
     if (p.n_chunks > 1) {
       const int nw = p.n_chunks * 5;
       unsigned long long* slot = p.slots + row * (long long)nw;
       if (tid == 0) {
+        const unsigned tag = offset ? kTagOffset : kTagFast;
         unsigned long long* mine = slot + c * 5;
-        __hip_atomic_store(mine + 0, tagged(m2s), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-        __hip_atomic_store(mine + 1, tagged(ss), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-        __hip_atomic_store(mine + 2, tagged(aa), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-        __hip_atomic_store(mine + 3, tagged(m2t), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-        __hip_atomic_store(mine + 4, tagged(st), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        __hip_atomic_store(mine + 0, tagged(m2s, tag), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        __hip_atomic_store(mine + 1, tagged(ss, tag), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        __hip_atomic_store(mine + 2, tagged(aa, tag), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        __hip_atomic_store(mine + 3, tagged(m2t, tag), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        __hip_atomic_store(mine + 4, tagged(st, tag), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
       }
       for (int q = tid; q < nw; q += kRowThreads) {
         unsigned long long x;
@@ -386,6 +462,7 @@ __global__ __launch_bounds__(kRowThreads) void rowkl_kernel(RowParams p) {
           __builtin_amdgcn_s_sleep(2);
         }
         s_part[q] = __uint_as_float((unsigned)x);
+        if (q % 5 == 0) s_tag[q / 5] = (unsigned)(x >> 32);
       }
       __syncthreads();
       if (s_timeout) {
@@ -393,53 +470,110 @@ __global__ __launch_bounds__(kRowThreads) void rowkl_kernel(RowParams p) {
         drain_stores();
         return;
       }
-      rm2s = -INFINITY;
-      rm2t = -INFINITY;
-      for (int k = 0; k < p.n_chunks; ++k) {
-        rm2s = fmaxf(rm2s, s_part[5 * k + 0]);
-        rm2t = fmaxf(rm2t, s_part[5 * k + 3]);
+      // every thread merges all chunks in chunk order (uniform branches):
+      // unrolled for the usual handful of chunks, a loop beyond
+      constexpr int kUnrolled = 8;
+#define TURNKL_TAG(K) (__builtin_amdgcn_readfirstlane(s_tag[K]) == kTagOffset)
+      r_s = -INFINITY;
+      r_t = -INFINITY;
+#pragma unroll
+      for (int k = 0; k < kUnrolled; ++k) {
+        if (k < p.n_chunks) {
+          const bool o = TURNKL_TAG(k);
+          row_offset = row_offset || o;
+          r_s = fmaxf(r_s, natural_ref(o, s_part[5 * k]));
+          r_t = fmaxf(r_t, natural_ref(o, s_part[5 * k + 3]));
+        }
       }
-      rss = 0.0f;
-      raa = 0.0f;
-      rst = 0.0f;
-      for (int k = 0; k < p.n_chunks; ++k) {
-        const float fs = exp2f(s_part[5 * k + 0] - rm2s);
-        const float ft = exp2f(s_part[5 * k + 3] - rm2t);
-        rss = fmaf(s_part[5 * k + 1], fs, rss);
-        raa = fmaf(s_part[5 * k + 2], fs, raa);
-        rst = fmaf(s_part[5 * k + 4], ft, rst);
+#pragma unroll 1
+      for (int k = kUnrolled; k < p.n_chunks; ++k) {
+        const bool o = TURNKL_TAG(k);
+        row_offset = row_offset || o;
+        r_s = fmaxf(r_s, natural_ref(o, s_part[5 * k]));
+        r_t = fmaxf(r_t, natural_ref(o, s_part[5 * k + 3]));
       }
+      const float d_r = r_s - r_t;
+#pragma unroll
+      for (int k = 0; k < kUnrolled; ++k) {
+        if (k < p.n_chunks) {
+          const float* w = s_part + 5 * k;
+          merge_chunk(TURNKL_TAG(k), w[0], w[1], w[2], w[3], w[4], r_s, r_t, d_r, r);
+        }
+      }
+#pragma unroll 1
+      for (int k = kUnrolled; k < p.n_chunks; ++k) {
+        const float* w = s_part + 5 * k;
+        merge_chunk(TURNKL_TAG(k), w[0], w[1], w[2], w[3], w[4], r_s, r_t, d_r, r);
+      }
+#undef TURNKL_TAG
+    } else {
+      r_s = natural_ref(offset, m2s);
+      r_t = natural_ref(offset, m2t);
+      merge_chunk(offset, m2s, ss, aa, m2t, st, r_s, r_t, r_s - r_t, r);
     }
-    const float mu = raa / rss;
-    if (c == 0 && tid == 0) p.kl[row] = mu + kLn2 * ((rm2t - rm2s) + log2f(rst / rss));
+    // mu = <p_s, (a - R_s) - (b - R_t)>;  KL = mu - lse(a - R_s) + lse(b - R_t)
+    const float mu = r.aa / r.ss;
+    if (c == 0 && tid == 0) p.kl[row] = mu + kLn2 * log2f(r.st / r.ss);
 
     // ---- gradient chunk, straight from registers:
-    // G = grad_scale * w * 2^(a log2e - lse2_s) * ((a - b) - mu), with
-    // log2 |grad_scale * w| folded into the exponent and the sign applied last
+    // G = grad_scale * w * 2^((a - R_s) log2e - log2 S_s) * ((a - R_s) - (b - R_t) - mu),
+    // with log2 |grad_scale * w| folded into the exponent and the sign applied
+    // last.  Ordinary rows fold R_s into the exponent's FMA and R_s - R_t into
+    // mu; rows that took the offset path subtract them per element.
     if (p.grad) {
       const float sc = p.wsc[row];
-      const float shift = (rm2s + log2f(rss)) - log2f(fabsf(sc));
+      const float l2 = log2f(r.ss) - log2f(fabsf(sc));
+      const float shift = row_offset ? l2 : fmaf(r_s, kLog2e, l2);
+      const float mu_g = row_offset ? mu : mu + (r_s - r_t);
       const unsigned flip = sc < 0.0f ? 0x80008000u : 0u;
-      const auto rg = chunk_rsrc(static_cast<char*>(p.grad) + (row * p.ld_g + pack_lo * kEpv) * kEs);
-      typename P::Data prev = P::zero();
+      const auto rg = chunk_rsrc(static_cast<char*>(p.grad) + (row * p.ld_g + col) * kEs);
+      if (!row_offset) {
+        typename P::Data prev = P::zero();
 #pragma unroll
-      for (int v = 0; v < kVpt; ++v) {
-        float out[kEpv];
+        for (int v = 0; v < kVpt; ++v) {
+          float out[kEpv];
 #pragma unroll
-        for (int j = 0; j < kEpv; ++j) {
-          const float a = xs[v].get(j);
-          const float b = xt[v].get(j);
-          out[j] = exp2_fast(fmaf(a, kLog2e, -shift)) * ((a - b) - mu);
+          for (int j = 0; j < kEpv; ++j) {
+            const float a = xs[v].get(j);
+            const float b = xt[v].get(j);
+            out[j] = exp2_fast(fmaf(a, kLog2e, -shift)) * ((a - b) - mu_g);
+          }
+          const typename P::Data cur = P::encode(out, flip);
+          if (valid[v]) P::store(rg, lane_off, v * kStep, cur);
+          // keep the store here, so the next pack's work separates it from
+          // any reuse of its data registers; the previous pack's data is free
+          __builtin_amdgcn_sched_barrier(0);
+          keep_alive(prev);
+          prev = cur;
         }
-        const typename P::Data cur = P::encode(out, flip);
-        if (valid[v]) P::store(rg, lane_off, v * kStep, cur);
-        // keep the store here, so the next pack's work separates it from any
-        // reuse of its data registers; the previous pack's data is free now
-        __builtin_amdgcn_sched_barrier(0);
-        keep_alive(prev);
-        prev = cur;
+        carry = prev;
+      } else {
+        // Offset rows (rare): read the chunk again, one pack at a time, so
+        // this loop keeps no unpacked values of the unrolled one alive.  Each
+        // thread reads a pack before it writes the same pack, which keeps an
+        // in-place gradient safe; every store is drained before its data
+        // registers can be reused.
+        const auto rs2 = chunk_rsrc(static_cast<const char*>(p.zs) + (row * p.ld_s + col) * kEs);
+        const auto rt2 = chunk_rsrc(static_cast<const char*>(p.zt) + (row * p.ld_t + col) * kEs);
+        keep_alive(carry);
+#pragma unroll 1
+        for (int v = 0; v < kVpt; ++v) {
+          if (v * kRowThreads + tid >= n_valid) break;
+          P ya, yb;
+          ya.load(rs2, lane_off, v * kStep);
+          yb.load(rt2, lane_off, v * kStep);
+          float out[kEpv];
+#pragma unroll
+          for (int j = 0; j < kEpv; ++j) {
+            const float a = ya.get(j) - r_s;
+            const float b = yb.get(j) - r_t;
+            out[j] = exp2_fast(fmaf(a, kLog2e, -shift)) * ((a - b) - mu_g);
+          }
+          P::store(rg, lane_off, v * kStep, P::encode(out, flip));
+          drain_stores();
+        }
+        carry = P::zero();
       }
-      carry = prev;
     }
     __syncthreads();
   }
@@ -469,7 +603,7 @@ hipError_t launch_one(const RowParams& p, hipStream_t s) {
       n = 1;
     return n;
   }();
-  const long long tasks = p.n_rows * (long long)p.n_chunks;
+  const long long tasks = (long long)p.n_rows * p.n_chunks;
   long long grid = (long long)occ * cu_count();
   if (grid > tasks) grid = tasks;
   if (grid < 1) return hipSuccess;

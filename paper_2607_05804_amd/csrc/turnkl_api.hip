@@ -16,6 +16,11 @@ thread_local int t_vpt_override = 0;
 
 bool vpt_allowed(int v) { return v >= 1 && v <= 16; }
 
+// Default cap on packs per thread: up to 13 packs of both rows stay within
+// 168 VGPRs, i.e. three waves per SIMD, which measured fastest (at V = 151936
+// it gives 6 chunks of at most 13 packs per thread).
+constexpr int kDefaultVmax = 13;
+
 long long ceil_div(long long a, long long b) { return (a + b - 1) / b; }
 }  // namespace
 
@@ -29,7 +34,7 @@ RowTiling vector_tiling(long long vocab, int dtype, int vmax) {
   RowTiling t{};
   t.vector = true;
   t.epv = dtype == TURNKL_BF16 ? 8 : 4;
-  if (vmax == 0) vmax = 16;
+  if (vmax == 0) vmax = kDefaultVmax;
   const long long packs = ceil_div(vocab, t.epv);
   t.n_chunks = (int)ceil_div(packs, (long long)kRowThreads * vmax);
   const long long widest = ceil_div(packs, t.n_chunks);
@@ -125,7 +130,10 @@ int turnkl_fwd_bwd(const void* student_logits, int64_t ld_student, const void* t
     ok = ok && packs / tiling.n_chunks >= (long long)kRowThreads * (tiling.vpt - 1);
     if (!ok) tiling = scalar_tiling(vocab);
   }
-  if (tiling.n_chunks * 5 > kMaxPartialWords) return TURNKL_ERR_INVALID_ARG;
+  if (tiling.n_chunks > kMaxChunks) return TURNKL_ERR_INVALID_ARG;
+  if (n_tokens > 0 && (ld_student > 0x7FFFFFFFll || ld_teacher > 0x7FFFFFFFll ||
+                       (grad_out && ld_grad > 0x7FFFFFFFll)))
+    return TURNKL_ERR_INVALID_ARG;
   if ((unsigned long long)n_tokens * (unsigned long long)tiling.n_chunks > 0x7FFFFFFFull)
     return TURNKL_ERR_INVALID_ARG;
 
@@ -142,18 +150,18 @@ int turnkl_fwd_bwd(const void* student_logits, int64_t ld_student, const void* t
 
   RowParams rp{};
   rp.zs = student_logits;
-  rp.ld_s = ld_student;
+  rp.ld_s = (int)ld_student;
   rp.zt = teacher_logits;
-  rp.ld_t = ld_teacher;
+  rp.ld_t = (int)ld_teacher;
   rp.grad = grad_out;
-  rp.ld_g = ld_grad;
+  rp.ld_g = grad_out ? (int)ld_grad : 0;
   rp.mask = loss_mask;
   rp.wsc = ws.wsc;
   rp.kl = kl;
   rp.hdr = ws.hdr;
   rp.slots = ws.slots;
-  rp.n_rows = n_tokens;
-  rp.vocab = vocab;
+  rp.n_rows = (int)n_tokens;
+  rp.n_packs = (int)(vocab / tiling.epv);
   rp.n_chunks = tiling.n_chunks;
   rp.bf16 = dtype == TURNKL_BF16;
   const bool prof = t_row_before && t_row_after;

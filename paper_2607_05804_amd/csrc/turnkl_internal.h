@@ -149,7 +149,8 @@ inline Ws bind(void* base, const Layout& L) {
 
 constexpr int kRowThreads = 256;
 constexpr int kScalarVpt = 32;         // elements per thread on the unaligned path
-constexpr int kMaxPartialWords = 640;  // LDS words for exchanged partials (n_chunks * 5)
+constexpr int kMaxChunks = 128;                 // chunks per row
+constexpr int kMaxPartialWords = kMaxChunks * 5;  // LDS words for exchanged partials
 
 struct RowTiling {
   bool vector;  // 16-byte vector loads (aligned rows, vocab a multiple of the vector)
@@ -179,21 +180,23 @@ hipError_t launch_segments(const SegParams& p, const Ws& ws, long long nblk, hip
 hipError_t launch_weights(const SegParams& p, const Ws& ws, double alpha, float grad_scale,
                           int n_chunks, float* kl, hipStream_t s);
 
+// Sizes are 32-bit here (the host rejects larger ones): the row kernel's
+// scalar registers are its scarcest resource.
 struct RowParams {
   const void* zs;
-  long long ld_s;
   const void* zt;
-  long long ld_t;
   void* grad;
-  long long ld_g;
   const unsigned char* mask;
   const float* wsc;
   float* kl;
   Header* hdr;
   unsigned long long* slots;
-  long long n_rows;
-  long long vocab;
-  int n_chunks;
+  int ld_s;
+  int ld_t;
+  int ld_g;
+  int n_rows;
+  int n_packs;   // vocab / elements per pack
+  int n_chunks;  // <= kMaxChunks
   int bf16;
 };
 

@@ -301,6 +301,51 @@ def test_extreme_but_finite_logits(gpu):
     check_all(out, ref, mask, 1.0, rows)
 
 
+def _as(dtype, x):
+    return bf16_bits(x) if dtype == "bf16" else np.asarray(x, np.float32)
+
+
+@pytest.mark.parametrize("dtype,vpt", [("f32", 0), ("bf16", 0), ("bf16", 2)])
+def test_spike_beyond_the_sampled_reference(dtype, vpt, gpu):
+    """One logit far above every thread's first pack overflows the fast
+    path's sums (2^(150 log2 e) > FLT_MAX); the chunk is redone against its
+    exact maximum."""
+    traj, turn, mask, zs, zt = make_batch(44, V=32000, dtype="f32")
+    rng = np.random.default_rng(7)
+    n = zs.shape[0]
+    cols = rng.integers(4096, 32000, n)
+    r = np.arange(n)
+    zs[r[0::3], cols[0::3]] += 150.0
+    zt[r[1::3], cols[1::3]] += 150.0
+    zs[r[2::3], cols[2::3]] += 150.0
+    zt[r[2::3], cols[2::3]] += 149.0
+    out, ref, rows = run_both(traj, turn, mask, _as(dtype, zs), _as(dtype, zt), vpt=vpt)
+    check_all(out, ref, mask, 1.0, rows)
+
+
+@pytest.mark.parametrize("dtype,vpt", [("bf16", 2), ("f32", 1), ("bf16", 0)])
+def test_rows_mixing_fast_and_offset_chunks(dtype, vpt, gpu):
+    """Row offsets of 50..69: some chunks of a row see a sampled maximum above
+    64 and take the offset path, their row mates do not; the merge and the
+    gradient must treat both forms alike."""
+    traj, turn, mask, zs, zt = make_batch(45, V=32000, dtype="f32")
+    off = (50.0 + np.arange(zs.shape[0]) % 20)[:, None].astype(np.float32)
+    out, ref, rows = run_both(traj, turn, mask, _as(dtype, zs + off), _as(dtype, zt + off + 0.5),
+                              vpt=vpt)
+    check_all(out, ref, mask, 1.0, rows)
+
+
+@pytest.mark.parametrize("shift_s,shift_t,dtype", [(5000.0, 5000.0, "f32"), (-3000.0, 3000.0, "f32"),
+                                                   (1000.0, 1000.0, "bf16"), (-96.0, 0.0, "bf16")])
+def test_large_logit_offsets_keep_full_accuracy(shift_s, shift_t, dtype, gpu):
+    """KL and its gradient do not depend on a constant added to a row of
+    either model; computed against the chunk references they keep the same
+    accuracy however large the offsets are."""
+    traj, turn, mask, zs, zt = make_batch(46, V=4096, dtype="f32")
+    out, ref, rows = run_both(traj, turn, mask, _as(dtype, zs + shift_s), _as(dtype, zt + shift_t))
+    check_all(out, ref, mask, 1.0, rows)
+
+
 # ----------------------------------------------------------------------------
 # data errors detected on the device
 
