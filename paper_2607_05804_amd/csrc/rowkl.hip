@@ -176,6 +176,14 @@ struct Pack<false, 1> {  // one fp32
 
 __device__ inline float exp2_fast(float x) { return __builtin_amdgcn_exp2f(x); }
 
+// Take a ticket: an atomic increment, which the compiler issues as one plain
+// global atomic whose result is waited for only where it is used (an atomic
+// add from one lane is rewritten into a wave-aggregated form that waits at
+// once).
+__device__ inline unsigned take_ticket(unsigned* counter) {
+  return __builtin_amdgcn_atomic_inc32(counter, 0xFFFFFFFFu, __ATOMIC_RELAXED, "agent");
+}
+
 // Exchange word: the tag in the high half marks it written and says how the
 // chunk's partials are expressed (kTagFast / kTagOffset); value in the low half.
 constexpr unsigned kTagFast = 1;
@@ -184,44 +192,70 @@ __device__ inline unsigned long long tagged(float v, unsigned tag) {
   return ((unsigned long long)tag << 32) | (unsigned long long)__float_as_uint(v);
 }
 
-// Row merge.  A chunk reports (M_s, S_s, A, M_t, S_t) in one of two forms:
-//  fast (tag kTagFast): M in log2 units (logits times log2 e),
+// Row merge.  A chunk reports (M_s, S_s, A, M_t, S_t, C_a, C_b) in one of two
+// forms:
+//  fast (tag kTagFast): M in log2 units (logits times log2 e), C = (0, 0),
 //    S_s = sum 2^(a log2e - M_s),  A = sum 2^(a log2e - M_s) (a - b),  S_t likewise;
-//  offset (kTagOffset): M in logit units,
-//    S_s = sum 2^((a - M_s) log2e),  A = sum 2^((a - M_s) log2e) ((a - M_s) - (b - M_t)).
+//  offset (kTagOffset): M = the chunk's maxima in logit units, C = (a, b)
+//    where the student's logit peaks in the chunk,
+//    S_s = sum 2^((a - M_s) log2e),  A = sum 2^((a - M_s) log2e) ((a - b) - (C_a - C_b)),
+//    with both differences taken exactly (two_diff), so a term is accurate
+//    to a few ulps of its own size whatever the magnitude of the logits.
+// The maxima are the references of the exponents; C is the reference of the
+// difference a - b, taken where the student's probability mass sits, so that
+// a spike in the teacher (which sets its maximum) does not inflate every
+// other term, and a peaked row's KL does not come from cancelling terms.
 // The row works against natural references (R_s, R_t) >= every chunk's
-// reference and accumulates, in chunk order,
+// reference and the difference reference C* of the offset chunk with the
+// largest C_a ((0, 0) when all chunks are fast), and accumulates in chunk order
 //   S_s = sum_v 2^((a_v - R_s) log2e),  S_t likewise,
-//   A   = sum_v 2^((a_v - R_s) log2e) ((a_v - R_s) - (b_v - R_t)),
-// so no term carries the magnitude of the logits: KL = A / S_s + ln(S_t / S_s).
-// A fast chunk scales by 2^(M_s - R_s log2e) (one FMA for the exponent) and
-// its A becomes A - S_s (R_s - R_t), which costs an error of ~u |R_s - R_t|;
-// an offset chunk scales by 2^((M_s - R_s) log2e) and gains
-// S_s ((M_s - R_s) - (M_t - R_t)), both differences small.
+//   A   = sum_v 2^((a_v - R_s) log2e) ((a_v - b_v) - (C*_a - C*_b)),
+// so that KL = A / S_s + ((C*_a - R_s) - (C*_b - R_t)) + ln(S_t / S_s).
+// A fast chunk scales by 2^(M_s - R_s log2e) (one FMA for the exponent), an
+// offset chunk by 2^((M_s - R_s) log2e); both add
+// S_s ((C_a - C_b) - (C*_a - C*_b)) to A (exact differences), zero for rows of
+// fast chunks only.
 struct RowSums {
   float ss, aa, st;
 };
 
+// Error-free difference (Knuth's TwoSum applied to x + (-y)): hi = fl(x - y)
+// and hi + lo = x - y exactly.  Needs plain rounded adds, which this file
+// guarantees (no contraction).
+struct Float2 {
+  float hi, lo;
+};
+__device__ inline Float2 two_diff(float x, float y) {
+  const float hi = x - y;
+  const float yv = hi - x;   // the part of hi that came from -y
+  const float xv = hi - yv;  // the part of hi that came from x
+  return Float2{hi, (x - xv) - (y + yv)};
+}
+
+// (x - y) - c for a double-float c, to within a few ulps of the result even
+// when x - y and c are large and nearly equal.
+__device__ inline float diff_minus(float x, float y, Float2 c) {
+  const Float2 d = two_diff(x, y);
+  return (d.hi - c.hi) + (d.lo - c.lo);
+}
+
 // natural reference of a chunk: a logit-unit value at or above its own
 __device__ inline float natural_ref(bool offset, float m) { return offset ? m : m * kLn2; }
 
-__device__ inline void merge_chunk(bool offset, float ms, float ss, float aa, float mt, float st,
-                                   float rs, float rt, float d_r, RowSums& r) {
+__device__ inline void merge_chunk(bool offset, const float* w, float rs, float rt, Float2 c_row,
+                                   RowSums& r) {
   float fs, ft;
   if (offset) {
-    const float ds = ms - rs;
-    const float dt = mt - rt;
-    fs = exp2f(ds * kLog2e);
-    ft = exp2f(dt * kLog2e);
-    aa = fmaf(ss, ds - dt, aa);
+    fs = exp2f((w[0] - rs) * kLog2e);
+    ft = exp2f((w[3] - rt) * kLog2e);
   } else {
-    fs = exp2f(fmaf(-rs, kLog2e, ms));
-    ft = exp2f(fmaf(-rt, kLog2e, mt));
-    aa = fmaf(-ss, d_r, aa);
+    fs = exp2f(fmaf(-rs, kLog2e, w[0]));
+    ft = exp2f(fmaf(-rt, kLog2e, w[3]));
   }
-  r.ss = fmaf(ss, fs, r.ss);
+  const float aa = fmaf(w[1], diff_minus(w[5], w[6], c_row), w[2]);
+  r.ss = fmaf(w[1], fs, r.ss);
   r.aa = fmaf(aa, fs, r.aa);
-  r.st = fmaf(st, ft, r.st);
+  r.st = fmaf(w[4], ft, r.st);
 }
 
 // One (row, chunk) task per iteration.  A chunk is the pack range
@@ -240,6 +274,7 @@ __global__ __launch_bounds__(kRowThreads) void rowkl_kernel(RowParams p) {
   __shared__ float s_sum[3][kRowWaves];
   __shared__ float s_part[kMaxPartialWords];
   __shared__ unsigned s_tag[kMaxChunks];
+  __shared__ float s_ref[kRowWaves];
   __shared__ int s_lo[kMaxChunks + 1];  // first pack of each chunk
   __shared__ unsigned s_task;
   __shared__ int s_timeout;
@@ -256,14 +291,25 @@ __global__ __launch_bounds__(kRowThreads) void rowkl_kernel(RowParams p) {
   // task's loads are issued (see keep_alive)
   typename P::Data carry = P::zero();
 
+  // Thread 0 takes the next ticket as soon as the current task can no longer
+  // wait on anyone (after its row merge, or at once for a masked row), so the
+  // atomic's latency hides behind the gradient.  A workgroup therefore never
+  // waits for row mates while it holds a ticket it has not started, which
+  // keeps the row-major ticket order deadlock-free.
+  constexpr unsigned kNoTicket = 0xFFFFFFFFu;
+  unsigned next_task = kNoTicket;
+
   for (;;) {
     if (tid == 0) {
-      s_task = atomicAdd(&p.hdr->ticket, 1u);
-      s_timeout = 0;
+      s_task = next_task != kNoTicket ? next_task : take_ticket(&p.hdr->ticket);
+      next_task = kNoTicket;
     }
     __syncthreads();
     const unsigned task = __builtin_amdgcn_readfirstlane(s_task);  // uniform: keep it scalar
     if (task >= n_tasks) break;
+    // s_task is rewritten only after every wave has passed a later barrier of
+    // this task (pass 1's, or the masked path's), so no wave can miss it
+    if (tid == 0) s_timeout = 0;
     const long long row = (long long)(task / (unsigned)p.n_chunks);
     const int c = (int)(task - (unsigned)row * (unsigned)p.n_chunks);
     const int pack_lo = __builtin_amdgcn_readfirstlane(s_lo[c]);
@@ -277,6 +323,7 @@ __global__ __launch_bounds__(kRowThreads) void rowkl_kernel(RowParams p) {
       valid[v] = (kCheckAll || v == kVpt - 1) ? (v * kRowThreads + tid < n_valid) : true;
 
     if (!p.mask[row]) {
+      if (tid == 0) next_task = take_ticket(&p.hdr->ticket);
       if (p.grad) {
         const typename P::Data z = P::zero();
         const auto rg = chunk_rsrc(static_cast<char*>(p.grad) + (row * p.ld_g + col) * kEs);
@@ -337,28 +384,28 @@ __global__ __launch_bounds__(kRowThreads) void rowkl_kernel(RowParams p) {
     xs[v].fence();                                       \
     xt[v].fence();                                       \
   }
-  // OFFSET (a literal): subtract natural references RS, RT per element;
-  // otherwise RS, RT are log2-unit references folded into the exponent FMA
-#define TURNKL_CHUNK_SUMS(OFFSET, RS, RT, SS, AA, ST)                         \
+  // OFFSET (a literal): exponents against natural references RS, RT and the
+  // exact difference against the double-float C2; otherwise RS, RT are
+  // log2-unit references folded into the exponent FMA (C2 unused)
+#define TURNKL_CHUNK_SUMS(OFFSET, RS, RT, C2, SS, AA, ST)                     \
   {                                                                           \
     SS = 0.0f;                                                                \
     AA = 0.0f;                                                                \
     ST = 0.0f;                                                                \
     _Pragma("unroll") for (int v = 0; v < kVpt; ++v) {                        \
       _Pragma("unroll") for (int j = 0; j < kEpv; ++j) {                      \
-        float a = xs[v].get(j);                                               \
-        float b = xt[v].get(j);                                               \
-        float es, et;                                                         \
+        const float a = xs[v].get(j);                                         \
+        const float b = xt[v].get(j);                                         \
+        float es, et, d;                                                      \
         if (OFFSET) {                                                         \
-          a -= (RS);                                                          \
-          b -= (RT);                                                          \
-          es = exp2_fast(a * kLog2e);                                         \
-          et = exp2_fast(b * kLog2e);                                         \
+          es = exp2_fast((a - (RS)) * kLog2e);                                \
+          et = exp2_fast((b - (RT)) * kLog2e);                                \
+          d = diff_minus(a, b, (C2));                                         \
         } else {                                                              \
           es = exp2_fast(fmaf(a, kLog2e, -(RS)));                             \
           et = exp2_fast(fmaf(b, kLog2e, -(RT)));                             \
+          d = a - b;                                                          \
         }                                                                     \
-        float d = a - b;                                                      \
         if (kCheckAll || v == kVpt - 1) {                                     \
           es = valid[v] ? es : 0.0f;                                          \
           et = valid[v] ? et : 0.0f;                                          \
@@ -399,28 +446,64 @@ __global__ __launch_bounds__(kRowThreads) void rowkl_kernel(RowParams p) {
     float m2t = mt * kLog2e;
     TURNKL_FENCE_ALL()
     float ss, aa, st;
-    TURNKL_CHUNK_SUMS(false, m2s, m2t, ss, aa, st)
+    float c_a = 0.0f, c_b = 0.0f;  // difference reference (offset form only)
+    TURNKL_CHUNK_SUMS(false, m2s, m2t, Float2{}, ss, aa, st)
     const bool offset = !(fmaxf(fabsf(m2s), fabsf(m2t)) <= kFar2) ||
                         !(__builtin_isfinite(ss) && __builtin_isfinite(st));
     if (offset) {
       __syncthreads();  // s_max / s_sum are about to be reused
       TURNKL_FENCE_ALL()
+      // exact maxima, and the teacher logit at the student's maximum (ties:
+      // the larger teacher logit, so every combination order agrees)
       ms = -INFINITY;
       mt = -INFINITY;
+      float bm = -INFINITY;
 #pragma unroll
       for (int v = 0; v < kVpt; ++v) {
 #pragma unroll
         for (int j = 0; j < kEpv; ++j) {
-          ms = fmaxf(ms, valid[v] ? xs[v].get(j) : -INFINITY);
-          mt = fmaxf(mt, valid[v] ? xt[v].get(j) : -INFINITY);
+          const float a = valid[v] ? xs[v].get(j) : -INFINITY;
+          const float b = valid[v] ? xt[v].get(j) : -INFINITY;
+          const bool take = (a > ms) | ((a == ms) & (b > bm));  // branch-free
+          ms = take ? a : ms;
+          bm = take ? b : bm;
+          mt = fmaxf(mt, b);
         }
       }
-      TURNKL_BLOCK_MAX2(ms, mt)
+#pragma unroll
+      for (int o = kWave / 2; o > 0; o >>= 1) {
+        const float oa = __shfl_xor(ms, o, kWave);
+        const float ob = __shfl_xor(bm, o, kWave);
+        const bool take = (oa > ms) | ((oa == ms) & (ob > bm));
+        ms = take ? oa : ms;
+        bm = take ? ob : bm;
+        mt = fmaxf(mt, __shfl_xor(mt, o, kWave));
+      }
+      if (lane == 0) {
+        s_max[0][wid] = ms;
+        s_max[1][wid] = mt;
+        s_ref[wid] = bm;
+      }
+      __syncthreads();
+      ms = s_max[0][0];
+      mt = s_max[1][0];
+      bm = s_ref[0];
+#pragma unroll
+      for (int w = 1; w < kRowWaves; ++w) {
+        const float oa = s_max[0][w];
+        const float ob = s_ref[w];
+        const bool take = (oa > ms) | ((oa == ms) & (ob > bm));
+        ms = take ? oa : ms;
+        bm = take ? ob : bm;
+        mt = fmaxf(mt, s_max[1][w]);
+      }
       m2s = ms;  // from here on: natural references
       m2t = mt;
+      c_a = ms;  // difference reference: (a, b) where the student peaks
+      c_b = bm;
       TURNKL_FENCE_ALL()
       __syncthreads();
-      TURNKL_CHUNK_SUMS(true, m2s, m2t, ss, aa, st)
+      TURNKL_CHUNK_SUMS(true, m2s, m2t, two_diff(c_a, c_b), ss, aa, st)
     }
 #undef TURNKL_CHUNK_SUMS
 #undef TURNKL_FENCE_ALL
@@ -437,19 +520,19 @@ __global__ __launch_bounds__(kRowThreads) void rowkl_kernel(RowParams p) {
     // row computes the same bits.  If any chunk took the offset path, the
     // whole row writes its gradient with offsets too.
     RowSums r{0.0f, 0.0f, 0.0f};
-    float r_s, r_t;  // row references, logit units
+    float r_s, r_t;              // row references of the exponents, logit units
+    float d_s = 0.0f, d_t = 0.0f;  // row reference C* of the difference a - b
     bool row_offset = offset;
     if (p.n_chunks > 1) {
-      const int nw = p.n_chunks * 5;
+      const int nw = p.n_chunks * kExchangeWords;
       unsigned long long* slot = p.slots + row * (long long)nw;
       if (tid == 0) {
         const unsigned tag = offset ? kTagOffset : kTagFast;
-        unsigned long long* mine = slot + c * 5;
-        __hip_atomic_store(mine + 0, tagged(m2s, tag), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-        __hip_atomic_store(mine + 1, tagged(ss, tag), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-        __hip_atomic_store(mine + 2, tagged(aa, tag), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-        __hip_atomic_store(mine + 3, tagged(m2t, tag), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-        __hip_atomic_store(mine + 4, tagged(st, tag), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        unsigned long long* mine = slot + c * kExchangeWords;
+        const float words[kExchangeWords] = {m2s, ss, aa, m2t, st, c_a, c_b};
+#pragma unroll
+        for (int q = 0; q < kExchangeWords; ++q)
+          __hip_atomic_store(mine + q, tagged(words[q], tag), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
       }
       for (int q = tid; q < nw; q += kRowThreads) {
         unsigned long long x;
@@ -462,7 +545,7 @@ __global__ __launch_bounds__(kRowThreads) void rowkl_kernel(RowParams p) {
           __builtin_amdgcn_s_sleep(2);
         }
         s_part[q] = __uint_as_float((unsigned)x);
-        if (q % 5 == 0) s_tag[q / 5] = (unsigned)(x >> 32);
+        if (q % kExchangeWords == 0) s_tag[q / kExchangeWords] = (unsigned)(x >> 32);
       }
       __syncthreads();
       if (s_timeout) {
@@ -476,55 +559,57 @@ __global__ __launch_bounds__(kRowThreads) void rowkl_kernel(RowParams p) {
 #define TURNKL_TAG(K) (__builtin_amdgcn_readfirstlane(s_tag[K]) == kTagOffset)
       r_s = -INFINITY;
       r_t = -INFINITY;
+      row_offset = false;
+#define TURNKL_REFS(K)                                              \
+  {                                                                 \
+    const bool o = TURNKL_TAG(K);                                   \
+    const float* w = s_part + kExchangeWords * (K);                 \
+    if (o && (!row_offset || w[5] > d_s)) {                         \
+      d_s = w[5];                                                   \
+      d_t = w[6];                                                   \
+    }                                                               \
+    row_offset = row_offset || o;                                   \
+    r_s = fmaxf(r_s, natural_ref(o, w[0]));                         \
+    r_t = fmaxf(r_t, natural_ref(o, w[3]));                         \
+  }
 #pragma unroll
-      for (int k = 0; k < kUnrolled; ++k) {
-        if (k < p.n_chunks) {
-          const bool o = TURNKL_TAG(k);
-          row_offset = row_offset || o;
-          r_s = fmaxf(r_s, natural_ref(o, s_part[5 * k]));
-          r_t = fmaxf(r_t, natural_ref(o, s_part[5 * k + 3]));
-        }
-      }
+      for (int k = 0; k < kUnrolled; ++k)
+        if (k < p.n_chunks) TURNKL_REFS(k)
 #pragma unroll 1
-      for (int k = kUnrolled; k < p.n_chunks; ++k) {
-        const bool o = TURNKL_TAG(k);
-        row_offset = row_offset || o;
-        r_s = fmaxf(r_s, natural_ref(o, s_part[5 * k]));
-        r_t = fmaxf(r_t, natural_ref(o, s_part[5 * k + 3]));
-      }
-      const float d_r = r_s - r_t;
+      for (int k = kUnrolled; k < p.n_chunks; ++k) TURNKL_REFS(k)
+#undef TURNKL_REFS
+      const Float2 c_row = two_diff(d_s, d_t);
 #pragma unroll
-      for (int k = 0; k < kUnrolled; ++k) {
-        if (k < p.n_chunks) {
-          const float* w = s_part + 5 * k;
-          merge_chunk(TURNKL_TAG(k), w[0], w[1], w[2], w[3], w[4], r_s, r_t, d_r, r);
-        }
-      }
+      for (int k = 0; k < kUnrolled; ++k)
+        if (k < p.n_chunks) merge_chunk(TURNKL_TAG(k), s_part + kExchangeWords * k, r_s, r_t, c_row, r);
 #pragma unroll 1
-      for (int k = kUnrolled; k < p.n_chunks; ++k) {
-        const float* w = s_part + 5 * k;
-        merge_chunk(TURNKL_TAG(k), w[0], w[1], w[2], w[3], w[4], r_s, r_t, d_r, r);
-      }
+      for (int k = kUnrolled; k < p.n_chunks; ++k)
+        merge_chunk(TURNKL_TAG(k), s_part + kExchangeWords * k, r_s, r_t, c_row, r);
 #undef TURNKL_TAG
     } else {
       r_s = natural_ref(offset, m2s);
       r_t = natural_ref(offset, m2t);
-      merge_chunk(offset, m2s, ss, aa, m2t, st, r_s, r_t, r_s - r_t, r);
+      d_s = c_a;
+      d_t = c_b;
+      const float w[kExchangeWords] = {m2s, ss, aa, m2t, st, c_a, c_b};
+      merge_chunk(offset, w, r_s, r_t, two_diff(d_s, d_t), r);
     }
-    // mu = <p_s, (a - R_s) - (b - R_t)>;  KL = mu - lse(a - R_s) + lse(b - R_t)
+    if (tid == 0) next_task = take_ticket(&p.hdr->ticket);
+
+    // mu = <p_s, (a - b) - (C*_a - C*_b)>,
+    // KL = <p_s, a - b> - lse(a) + lse(b) = mu + ((C*_a - R_s) - (C*_b - R_t)) + ln(S_t / S_s)
     const float mu = r.aa / r.ss;
-    if (c == 0 && tid == 0) p.kl[row] = mu + kLn2 * log2f(r.st / r.ss);
+    if (c == 0 && tid == 0) p.kl[row] = (mu + ((d_s - r_s) - (d_t - r_t))) + kLn2 * log2f(r.st / r.ss);
 
     // ---- gradient chunk, straight from registers:
-    // G = grad_scale * w * 2^((a - R_s) log2e - log2 S_s) * ((a - R_s) - (b - R_t) - mu),
+    // G = grad_scale * w * 2^((a - R_s) log2e - log2 S_s) * (((a - b) - (C*_a - C*_b)) - mu),
     // with log2 |grad_scale * w| folded into the exponent and the sign applied
-    // last.  Ordinary rows fold R_s into the exponent's FMA and R_s - R_t into
-    // mu; rows that took the offset path subtract them per element.
+    // last.  Rows of fast chunks only (C* = 0) fold R_s into the exponent's
+    // FMA; rows with an offset chunk subtract the references per element.
     if (p.grad) {
       const float sc = p.wsc[row];
       const float l2 = log2f(r.ss) - log2f(fabsf(sc));
       const float shift = row_offset ? l2 : fmaf(r_s, kLog2e, l2);
-      const float mu_g = row_offset ? mu : mu + (r_s - r_t);
       const unsigned flip = sc < 0.0f ? 0x80008000u : 0u;
       const auto rg = chunk_rsrc(static_cast<char*>(p.grad) + (row * p.ld_g + col) * kEs);
       if (!row_offset) {
@@ -536,7 +621,7 @@ __global__ __launch_bounds__(kRowThreads) void rowkl_kernel(RowParams p) {
           for (int j = 0; j < kEpv; ++j) {
             const float a = xs[v].get(j);
             const float b = xt[v].get(j);
-            out[j] = exp2_fast(fmaf(a, kLog2e, -shift)) * ((a - b) - mu_g);
+            out[j] = exp2_fast(fmaf(a, kLog2e, -shift)) * ((a - b) - mu);
           }
           const typename P::Data cur = P::encode(out, flip);
           if (valid[v]) P::store(rg, lane_off, v * kStep, cur);
@@ -553,6 +638,7 @@ __global__ __launch_bounds__(kRowThreads) void rowkl_kernel(RowParams p) {
         // thread reads a pack before it writes the same pack, which keeps an
         // in-place gradient safe; every store is drained before its data
         // registers can be reused.
+        const Float2 c_row = two_diff(d_s, d_t);
         const auto rs2 = chunk_rsrc(static_cast<const char*>(p.zs) + (row * p.ld_s + col) * kEs);
         const auto rt2 = chunk_rsrc(static_cast<const char*>(p.zt) + (row * p.ld_t + col) * kEs);
         keep_alive(carry);
@@ -565,9 +651,9 @@ __global__ __launch_bounds__(kRowThreads) void rowkl_kernel(RowParams p) {
           float out[kEpv];
 #pragma unroll
           for (int j = 0; j < kEpv; ++j) {
-            const float a = ya.get(j) - r_s;
-            const float b = yb.get(j) - r_t;
-            out[j] = exp2_fast(fmaf(a, kLog2e, -shift)) * ((a - b) - mu_g);
+            const float a = ya.get(j);
+            const float b = yb.get(j);
+            out[j] = exp2_fast(fmaf(a - r_s, kLog2e, -shift)) * (diff_minus(a, b, c_row) - mu);
           }
           P::store(rg, lane_off, v * kStep, P::encode(out, flip));
           drain_stores();
@@ -575,7 +661,6 @@ __global__ __launch_bounds__(kRowThreads) void rowkl_kernel(RowParams p) {
         carry = P::zero();
       }
     }
-    __syncthreads();
   }
   drain_stores();
 }

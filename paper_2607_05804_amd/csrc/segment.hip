@@ -227,7 +227,7 @@ hipError_t launch_segments(const SegParams& p, const Ws& ws, long long nblk, hip
 hipError_t launch_weights(const SegParams& p, const Ws& ws, double alpha, float grad_scale,
                           int n_chunks, float* kl, hipStream_t s) {
   if (p.n == 0) return hipSuccess;
-  const int slot_words = n_chunks > 1 ? n_chunks * 5 : 0;
+  const int slot_words = n_chunks > 1 ? n_chunks * kExchangeWords : 0;
   token_weights<<<grid_for(p.n, kSegThreads, 4096), kSegThreads, 0, s>>>(p, ws, alpha, grad_scale,
                                                                          slot_words, kl);
   return hipGetLastError();

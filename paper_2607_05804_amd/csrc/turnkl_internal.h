@@ -69,6 +69,9 @@ struct Layout {
 
 inline size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
 
+// 64-bit words a row-kernel chunk publishes to its row mates
+constexpr int kExchangeWords = 7;
+
 inline Layout make_layout(long long n_tokens, int n_chunks) {
   Layout L{};
   const size_t n = (size_t)n_tokens;
@@ -93,7 +96,7 @@ inline Layout make_layout(long long n_tokens, int n_chunks) {
   L.wsc = take(n * 4);
   L.kl = take(n * 4);
   L.seg_stat = take(n * sizeof(SegStat));
-  L.slots = take(n * (size_t)n_chunks * 5 * 8);
+  L.slots = take(n * (size_t)n_chunks * kExchangeWords * 8);
   L.total = o;
   return L;
 }
@@ -150,7 +153,7 @@ inline Ws bind(void* base, const Layout& L) {
 constexpr int kRowThreads = 256;
 constexpr int kScalarVpt = 32;         // elements per thread on the unaligned path
 constexpr int kMaxChunks = 128;                 // chunks per row
-constexpr int kMaxPartialWords = kMaxChunks * 5;  // LDS words for exchanged partials
+constexpr int kMaxPartialWords = kMaxChunks * kExchangeWords;  // LDS words for exchanged partials
 
 struct RowTiling {
   bool vector;  // 16-byte vector loads (aligned rows, vocab a multiple of the vector)
