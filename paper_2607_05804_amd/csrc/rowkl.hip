@@ -61,6 +61,12 @@ constexpr float kFar2 = 64.0f * kLog2e;
 // per-lane VGPR part and a compile-time SGPR step.
 constexpr int kRsrcWord3 = 0x00020000;
 
+// Cache policy of the logit loads and gradient stores: non-temporal (the nt
+// bit of gfx940-family buffer instructions).  Every logit is read once and
+// every gradient element written once, so nothing is gained by keeping them
+// in L2; streaming them measured about 3% faster than the default policy.
+constexpr int kStream = 2;
+
 __device__ inline __amdgpu_buffer_rsrc_t chunk_rsrc(const void* base) {
   return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), 0, 0x7FFFFFFF, kRsrcWord3);
 }
@@ -86,7 +92,7 @@ struct Pack<true, 8> {  // 8 bf16 = 16 bytes
   using Data = u32x4;
   unsigned w[4];
   __device__ void load(__amdgpu_buffer_rsrc_t r, int voff, int soff) {
-    const auto u = __builtin_amdgcn_raw_buffer_load_b128(r, voff, soff, 0);
+    const auto u = __builtin_amdgcn_raw_buffer_load_b128(r, voff, soff, kStream);
     w[0] = u[0]; w[1] = u[1]; w[2] = u[2]; w[3] = u[3];
   }
   // Opaque to the optimiser: values unpacked before the fence cannot be
@@ -109,7 +115,7 @@ struct Pack<true, 8> {  // 8 bf16 = 16 bytes
   }
   __device__ static Data zero() { return Data{0u, 0u, 0u, 0u}; }
   __device__ static void store(__amdgpu_buffer_rsrc_t r, int voff, int soff, const Data& o) {
-    __builtin_amdgcn_raw_buffer_store_b128(o, r, voff, soff, 0);
+    __builtin_amdgcn_raw_buffer_store_b128(o, r, voff, soff, kStream);
   }
 };
 
@@ -118,7 +124,7 @@ struct Pack<false, 4> {  // 4 fp32 = 16 bytes
   using Data = u32x4;
   float f[4];
   __device__ void load(__amdgpu_buffer_rsrc_t r, int voff, int soff) {
-    const auto u = __builtin_amdgcn_raw_buffer_load_b128(r, voff, soff, 0);
+    const auto u = __builtin_amdgcn_raw_buffer_load_b128(r, voff, soff, kStream);
     f[0] = __uint_as_float(u[0]); f[1] = __uint_as_float(u[1]);
     f[2] = __uint_as_float(u[2]); f[3] = __uint_as_float(u[3]);
   }
@@ -133,7 +139,7 @@ struct Pack<false, 4> {  // 4 fp32 = 16 bytes
   }
   __device__ static Data zero() { return Data{0u, 0u, 0u, 0u}; }
   __device__ static void store(__amdgpu_buffer_rsrc_t r, int voff, int soff, const Data& o) {
-    __builtin_amdgcn_raw_buffer_store_b128(o, r, voff, soff, 0);
+    __builtin_amdgcn_raw_buffer_store_b128(o, r, voff, soff, kStream);
   }
 };
 
@@ -142,7 +148,7 @@ struct Pack<true, 1> {  // one bf16
   using Data = unsigned;
   unsigned w;
   __device__ void load(__amdgpu_buffer_rsrc_t r, int voff, int soff) {
-    w = __builtin_amdgcn_raw_buffer_load_b16(r, voff, soff, 0);
+    w = __builtin_amdgcn_raw_buffer_load_b16(r, voff, soff, kStream);
   }
   __device__ void fence() { asm volatile("" : "+v"(w)); }
   __device__ float get(int) const { return __uint_as_float(w << 16); }
@@ -152,7 +158,7 @@ struct Pack<true, 1> {  // one bf16
   }
   __device__ static Data zero() { return 0u; }
   __device__ static void store(__amdgpu_buffer_rsrc_t r, int voff, int soff, const Data& o) {
-    __builtin_amdgcn_raw_buffer_store_b16((unsigned short)o, r, voff, soff, 0);
+    __builtin_amdgcn_raw_buffer_store_b16((unsigned short)o, r, voff, soff, kStream);
   }
 };
 
@@ -161,7 +167,7 @@ struct Pack<false, 1> {  // one fp32
   using Data = unsigned;
   float f;
   __device__ void load(__amdgpu_buffer_rsrc_t r, int voff, int soff) {
-    f = __uint_as_float(__builtin_amdgcn_raw_buffer_load_b32(r, voff, soff, 0));
+    f = __uint_as_float(__builtin_amdgcn_raw_buffer_load_b32(r, voff, soff, kStream));
   }
   __device__ void fence() { asm volatile("" : "+v"(f)); }
   __device__ float get(int) const { return f; }
@@ -170,7 +176,7 @@ struct Pack<false, 1> {  // one fp32
   }
   __device__ static Data zero() { return 0u; }
   __device__ static void store(__amdgpu_buffer_rsrc_t r, int voff, int soff, const Data& o) {
-    __builtin_amdgcn_raw_buffer_store_b32(o, r, voff, soff, 0);
+    __builtin_amdgcn_raw_buffer_store_b32(o, r, voff, soff, kStream);
   }
 };
 
