@@ -72,6 +72,42 @@ def cpu_baseline(w, sample_tokens: int):
                         f"before the clock starts), {dt:.1f} s"}
 
 
+def success_stand_in(w):
+    """Turn counts of the even-numbered trajectories, standing in for the
+    successful completions of a probe batch (the synthetic batch has none)."""
+    import numpy as np
+    return [int(np.unique(w.turn_id[w.traj_id == b]).size)
+            for b in np.unique(w.traj_id[w.traj_id >= 0]) if b % 2 == 0]
+
+
+def depth_controller_timing(T, stats, w, reps: int = 2000):
+    """Host time of one rollout-depth controller update (turnkl_depth_update,
+    Sec. 5.1) on this batch's per-turn statistics, ctypes call included."""
+    st = T.read_turn_stats(stats)
+    succ = success_stand_in(w)
+    ctl = T.DepthController()
+    t0 = time.perf_counter()
+    for _ in range(reps):
+        ctl.update(st, succ)
+    lib_us = (time.perf_counter() - t0) / reps * 1e6
+    return {"update_us": lib_us, "turns": int(st.shape[0]), "successes": len(succ),
+            "h_eff": ctl.state.h_eff, "h_cov": ctl.state.h_cov,
+            "cap_after_probe": ctl.plan(4)[0]}
+
+
+def oracle_controller_timing(stats_np, w, reps: int = 200):
+    """The oracle's controller update on the same statistics (CPU baseline)."""
+    from oracle import depth_controller as D
+    succ = success_stand_in(w)
+    cfg = D.Config()
+    st = D.init(cfg)
+    k, n = list(stats_np["kl_mean"]), list(stats_np["n_traj"])
+    t0 = time.perf_counter()
+    for _ in range(reps):
+        st = D.update(cfg, st, k, n, succ)
+    return (time.perf_counter() - t0) / reps * 1e6
+
+
 def copy_probe(gib: float, steps: int) -> int:
     """torch's device-to-device copy of a buffer of known size."""
     import torch
@@ -199,10 +235,13 @@ def main() -> int:
         },
         "step_hbm_gbs": row_bytes / (ms_per_step * 1e-3) / 1e9,
     }
+    out["depth_controller"] = depth_controller_timing(T, stats, w)
+    stats_np = T.read_turn_stats(stats)
     del zs, zt, grad
     torch.cuda.empty_cache()
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(w, args.cpu_sample_tokens)
+        out["cpu_baseline"]["depth_controller_update_us"] = oracle_controller_timing(stats_np, w)
     print(json.dumps(out), flush=True)
     return 0
 

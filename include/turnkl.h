@@ -198,6 +198,75 @@ int turnkl_profile_row_kernel(hipEvent_t before, hipEvent_t after);
  */
 int turnkl_set_row_tiling(int vectors_per_thread);
 
+/* ------------------------------------------------------------------------
+ * Adaptive rollout-depth controller (Sec. 5.1; App. D, Algorithm 1 and the
+ * full-configuration table).  HOST functions: all pointers are host memory,
+ * nothing touches the GPU.  They consume the per-turn statistics that
+ * turnkl_fwd_bwd wrote for a probe batch (after the caller copies the
+ * turnkl_turn_stat array to the host), and return the rollout depth cap that
+ * the rollout engine applies on the following steps.
+ *
+ * Turn indices are 0-based throughout; the cap adds 1 to turn an index into a
+ * number of turns.  round() is round-half-to-even.
+ *
+ *   probe batch   K_t = kl_mean[t], n_t = n_traj[t] of the batch's stats;
+ *   efficiency    m_t = [K_t]_+ n_t / n_0 (0 when n_0 = 0),
+ *                 q_t = m_t / (sum_j m_j + eps), H_eff = round(sum_t t q_t);
+ *   coverage      with L_i the turn counts of the batch's successful
+ *                 trajectories (or of all trajectories, for the paper's
+ *                 full-population variant), refreshed only when at least
+ *                 min_cov_traj of them are given:
+ *                 H_cov = min{H >= 0 : #{i : L_i - 1 <= H} / n >= p}
+ *                 (0 until first refreshed, then kept);
+ *   update        H_ctrl = max(H_eff, H_cov),
+ *                 Hbar_k = (1 - ema_alpha) Hbar_{k-1} + ema_alpha H_ctrl on
+ *                 probe steps (Hbar_0 = h_max), unchanged otherwise;
+ *   plan          cap_k = clip(round(Hbar_{k-1}) + 1, h_min, h_max); step k
+ *                 (k = 1, 2, ...) is a probe when k <= warmup_steps or
+ *                 k % probe_interval == 0; a probe rolls out to h_max, any
+ *                 other step to cap_k.
+ * ------------------------------------------------------------------------ */
+typedef struct {
+  int32_t h_min, h_max;        /* clamp of the applied cap (2, 50) */
+  int32_t warmup_steps;        /* steps 1..warmup_steps are probes (3) */
+  int32_t probe_interval;      /* and every probe_interval-th step (8) */
+  int32_t min_cov_traj;        /* successful trajectories needed to refresh H_cov (8) */
+  double coverage_quantile;    /* p in (0, 1] (0.80) */
+  double ema_alpha;            /* in [0, 1] (0.30); not the loss-blend alpha */
+  double eps;                  /* >= 0, guard of the q_t normaliser (1e-12) */
+} turnkl_depth_config;
+
+typedef struct {
+  double h_bar;      /* EMA of H_ctrl; h_max after init */
+  double h_eff_bar;  /* last centroid before rounding; -1 before the first probe */
+  int32_t h_eff;     /* last efficiency centroid; -1 before the first probe */
+  int32_t h_cov;     /* coverage floor; 0 until first refreshed */
+  int32_t h_ctrl;    /* last max(H_eff, H_cov); -1 before the first probe */
+  int32_t n_probes;  /* probe updates so far */
+} turnkl_depth_state;
+
+/* Fill `cfg` (host) with the values of App. D's configuration table. */
+void turnkl_depth_default_config(turnkl_depth_config* cfg);
+
+/* Initialise `st` (host) for `cfg`.  TURNKL_ERR_INVALID_ARG for a null pointer
+ * or a configuration outside the ranges above (h_min >= 1, h_max >= h_min,
+ * warmup_steps >= 0, probe_interval >= 1, min_cov_traj >= 0). */
+int turnkl_depth_init(const turnkl_depth_config* cfg, turnkl_depth_state* st);
+
+/* Step `step` (>= 1): the cap, whether the step is a probe (0/1) and the
+ * rollout depth to use (host outputs).  Does not modify the state. */
+int turnkl_depth_plan(const turnkl_depth_config* cfg, const turnkl_depth_state* st, int64_t step,
+                      int32_t* cap, int32_t* probe, int32_t* rollout_depth);
+
+/* One probe update.  `stats` (host) holds n_turns >= 1 entries of the probe
+ * batch's per-turn statistics; `success_lengths` (host, may be NULL when
+ * n_success == 0) the turn counts (>= 1) of its successful trajectories.
+ * TURNKL_ERR_INVALID_ARG for null pointers, bad sizes or a length < 1; the
+ * state is then left unchanged. */
+int turnkl_depth_update(const turnkl_depth_config* cfg, turnkl_depth_state* st,
+                        const turnkl_turn_stat* stats, int32_t n_turns,
+                        const int32_t* success_lengths, int64_t n_success);
+
 #ifdef __cplusplus
 }
 #endif

@@ -32,13 +32,30 @@ F32 = 1
 # Names of every entry point include/turnkl.h declares.
 EXPORTS = ("turnkl_workspace_bytes", "turnkl_fwd_bwd", "turnkl_get_status",
            "turnkl_get_segments", "turnkl_alpha_schedule", "turnkl_status_string",
-           "turnkl_profile_row_kernel", "turnkl_set_row_tiling")
+           "turnkl_profile_row_kernel", "turnkl_set_row_tiling",
+           "turnkl_depth_default_config", "turnkl_depth_init", "turnkl_depth_plan",
+           "turnkl_depth_update")
 
 STAT_DTYPE = np.dtype([("n_tokens", "<i8"), ("n_traj", "<i8"), ("kl_mean", "<f8"),
                        ("kl_m2", "<f8"), ("kl_var", "<f8"), ("loss_mass", "<f8")])
 STAT_FIELDS = 6  # int64, int64, 4 x float64 -> 48 bytes
 
 _lib = None
+
+
+class DepthConfig(ctypes.Structure):
+    """turnkl_depth_config (include/turnkl.h)."""
+    _fields_ = [("h_min", ctypes.c_int32), ("h_max", ctypes.c_int32),
+                ("warmup_steps", ctypes.c_int32), ("probe_interval", ctypes.c_int32),
+                ("min_cov_traj", ctypes.c_int32), ("coverage_quantile", ctypes.c_double),
+                ("ema_alpha", ctypes.c_double), ("eps", ctypes.c_double)]
+
+
+class DepthState(ctypes.Structure):
+    """turnkl_depth_state (include/turnkl.h)."""
+    _fields_ = [("h_bar", ctypes.c_double), ("h_eff_bar", ctypes.c_double),
+                ("h_eff", ctypes.c_int32), ("h_cov", ctypes.c_int32),
+                ("h_ctrl", ctypes.c_int32), ("n_probes", ctypes.c_int32)]
 
 
 class TurnKLError(RuntimeError):
@@ -76,6 +93,17 @@ def lib() -> ctypes.CDLL:
         l.turnkl_profile_row_kernel.argtypes = [c.c_void_p, c.c_void_p]
         l.turnkl_set_row_tiling.restype = c.c_int
         l.turnkl_set_row_tiling.argtypes = [c.c_int]
+        l.turnkl_depth_default_config.restype = None
+        l.turnkl_depth_default_config.argtypes = [c.POINTER(DepthConfig)]
+        l.turnkl_depth_init.restype = c.c_int
+        l.turnkl_depth_init.argtypes = [c.POINTER(DepthConfig), c.POINTER(DepthState)]
+        l.turnkl_depth_plan.restype = c.c_int
+        l.turnkl_depth_plan.argtypes = [c.POINTER(DepthConfig), c.POINTER(DepthState), c.c_int64,
+                                        c.POINTER(c.c_int32), c.POINTER(c.c_int32),
+                                        c.POINTER(c.c_int32)]
+        l.turnkl_depth_update.restype = c.c_int
+        l.turnkl_depth_update.argtypes = [c.POINTER(DepthConfig), c.POINTER(DepthState), c.c_void_p,
+                                          c.c_int32, c.c_void_p, c.c_int64]
         _lib = l
     return _lib
 
@@ -217,3 +245,45 @@ def new_turn_stats(max_turns: int, device="cuda") -> torch.Tensor:
 
 def read_turn_stats(buf: torch.Tensor) -> np.ndarray:
     return buf.cpu().numpy().view(STAT_DTYPE)
+
+
+def _check(rc: int, what: str) -> None:
+    if rc != OK:
+        raise TurnKLError(rc, what)
+
+
+class DepthController:
+    """The adaptive rollout-depth controller (turnkl_depth_*; host code).
+
+    plan(k) -> (cap, probe, rollout_depth) for step k = 1, 2, ...;
+    update(stats, success_lengths) after a probe step, with the probe batch's
+    per-turn statistics (the buffer turnkl_fwd_bwd filled, on any device, or
+    a STAT_DTYPE array) and the turn counts of its successful trajectories.
+    """
+
+    def __init__(self, **overrides):
+        l = lib()
+        self.config = DepthConfig()
+        l.turnkl_depth_default_config(ctypes.byref(self.config))
+        for k, v in overrides.items():
+            setattr(self.config, k, v)
+        self.state = DepthState()
+        _check(l.turnkl_depth_init(ctypes.byref(self.config), ctypes.byref(self.state)),
+               "turnkl_depth_init")
+
+    def plan(self, step: int):
+        cap, probe, roll = ctypes.c_int32(), ctypes.c_int32(), ctypes.c_int32()
+        _check(lib().turnkl_depth_plan(ctypes.byref(self.config), ctypes.byref(self.state), step,
+                                       ctypes.byref(cap), ctypes.byref(probe), ctypes.byref(roll)),
+               "turnkl_depth_plan")
+        return cap.value, bool(probe.value), roll.value
+
+    def update(self, stats, success_lengths=()) -> None:
+        if isinstance(stats, torch.Tensor):
+            stats = read_turn_stats(stats)
+        st = np.ascontiguousarray(stats, dtype=STAT_DTYPE)
+        ln = np.ascontiguousarray(np.asarray(success_lengths, dtype=np.int32))
+        _check(lib().turnkl_depth_update(ctypes.byref(self.config), ctypes.byref(self.state),
+                                         st.ctypes.data, st.shape[0],
+                                         ln.ctypes.data if ln.size else None, ln.size),
+               "turnkl_depth_update")
