@@ -190,11 +190,11 @@ int turnkl_profile_row_kernel(hipEvent_t before, hipEvent_t after);
  * row of V logits into ceil(V / (256 * e * n)) balanced chunks, one
  * workgroup of 256 threads per chunk, where e is the number of elements in a
  * 16-byte vector (8 bf16, 4 fp32) and n = vectors_per_thread is the most
- * vectors a thread holds (1 to 16; default 13).  Smaller n means more, smaller
+ * vectors a thread holds (1 to 25; default 25).  Smaller n means more, smaller
  * chunks per row.  0 restores the default.  The workspace size depends on it
  * (turnkl_workspace_bytes reads the same setting).  Results agree up to
  * floating-point summation order.  Returns TURNKL_ERR_INVALID_ARG for values
- * outside 0..16.
+ * outside 0..25.
  */
 int turnkl_set_row_tiling(int vectors_per_thread);
 

@@ -709,7 +709,9 @@ hipError_t launch_vpt(const RowParams& p, int vpt, hipStream_t s) {
     case n: return launch_one<kBf16, kEpv, n, false>(p, s);
     TURNKL_CASE(1) TURNKL_CASE(2) TURNKL_CASE(3) TURNKL_CASE(4) TURNKL_CASE(5) TURNKL_CASE(6)
     TURNKL_CASE(7) TURNKL_CASE(8) TURNKL_CASE(9) TURNKL_CASE(10) TURNKL_CASE(11) TURNKL_CASE(12)
-    TURNKL_CASE(13) TURNKL_CASE(14) TURNKL_CASE(15) TURNKL_CASE(16)
+    TURNKL_CASE(13) TURNKL_CASE(14) TURNKL_CASE(15) TURNKL_CASE(16) TURNKL_CASE(17) TURNKL_CASE(18)
+    TURNKL_CASE(19) TURNKL_CASE(20) TURNKL_CASE(21) TURNKL_CASE(22) TURNKL_CASE(23) TURNKL_CASE(24)
+    TURNKL_CASE(25)
 #undef TURNKL_CASE
     default: return hipErrorInvalidValue;
   }

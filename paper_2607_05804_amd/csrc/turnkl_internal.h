@@ -152,6 +152,7 @@ inline Ws bind(void* base, const Layout& L) {
 
 constexpr int kRowThreads = 256;
 constexpr int kScalarVpt = 32;         // elements per thread on the unaligned path
+constexpr int kMaxVpt = 25;            // packs per thread of the widest vector instantiation
 constexpr int kMaxChunks = 128;                 // chunks per row
 constexpr int kMaxPartialWords = kMaxChunks * kExchangeWords;  // LDS words for exchanged partials
 

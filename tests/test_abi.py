@@ -58,7 +58,7 @@ def test_workspace_bytes():
         T.set_row_tiling(0)
     assert c > a
     with pytest.raises(T.TurnKLError):
-        T.set_row_tiling(17)
+        T.set_row_tiling(26)
     with pytest.raises(T.TurnKLError):
         T.set_row_tiling(-1)
 
