@@ -108,6 +108,74 @@ def oracle_controller_timing(stats_np, w, reps: int = 200):
     return (time.perf_counter() - t0) / reps * 1e6
 
 
+def topk_timing(T, zs, zt, turn, traj, mask, w, steps: int, warmup: int, k: int = 50):
+    """The top-K variant (App. D's top-K reverse KL, teacher support K = 50)
+    on the same batch: teacher support from the device teacher logits, dense
+    bf16 gradient out of place.  Its traffic is the dense gradient write plus
+    the support reads, so it is bound by HBM writes."""
+    import numpy as np
+    import torch
+    top_v, top_i = torch.topk(zt, k, dim=1)
+    ids = top_i.to(torch.int32).contiguous()
+    vals = top_v.float().contiguous()
+    del top_v, top_i
+    n, V = zs.shape
+    grad = torch.empty_like(zs)
+    stats = T.new_turn_stats(w.max_turns)
+    ws = T.TopkWorkspace(n, k, w.max_turns)
+
+    def step():
+        return T.fwd_bwd_topk(zs, ids, vals, turn, traj, mask, w.alphas[0], grad=grad,
+                              max_turns=w.max_turns, turn_stats=stats, workspace=ws, check=False)
+
+    for _ in range(warmup):
+        step()
+    torch.cuda.synchronize()
+    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+          for _ in range(steps)]
+    for a, b in ev:
+        a.record()
+        b.record()
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for a, b in ev:
+        T.profile_row_kernel(a, b)
+        step()
+    T.profile_row_kernel(None, None)
+    torch.cuda.synchronize()
+    elapsed = time.perf_counter() - t0
+    if ws.status() != T.OK:
+        raise RuntimeError(T.status_string(ws.status()))
+    kern_ms = float(np.mean([a.elapsed_time(b) for a, b in ev]))
+    n_sup = int(w.n_supervised)
+    by = n * V * 2 + n_sup * k * (4 + 4 + 2)
+    out = {"k": k, "tokens_per_s": n * steps / elapsed, "ms_per_step": elapsed * 1e3 / steps,
+           "kernels_ms": kern_ms, "algorithmic_bytes_per_call": by,
+           "roofline": {"bound": "hbm", "achieved": by / (kern_ms * 1e-3) / 1e9,
+                        "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                        "frac": by / (kern_ms * 1e-3) / 1e9 / HBM_PEAK_GBS},
+           "gradient": "dense bf16, out of place (zero off the support)"}
+    host = (ids.cpu().numpy(), vals.cpu().numpy())
+    idx = ids.long()
+    zs_at = torch.gather(zs, 1, idx).view(torch.int16).cpu().numpy().view(np.uint16)
+    del grad, idx, ws
+    torch.cuda.empty_cache()
+    return out, host + (zs_at,)
+
+
+def oracle_topk_timing(w, host):
+    """The top-K oracle on the whole batch (CPU baseline of the top-K path)."""
+    from oracle import topk_oracle as K
+    from oracle import turnkl_oracle as O
+    ids, vals, zs_at = host
+    t0 = time.perf_counter()
+    ref = K.fwd_bwd_topk(w.traj_id, w.turn_id, w.loss_mask, w.alphas[0], w.max_turns,
+                         lambda r, i: zs_at[r], ids, vals, O.DTYPE_BF16)
+    dt = time.perf_counter() - t0
+    assert ref.status == O.OK
+    return w.n_tokens / dt
+
+
 def copy_probe(gib: float, steps: int) -> int:
     """torch's device-to-device copy of a buffer of known size."""
     import torch
@@ -237,11 +305,15 @@ def main() -> int:
     }
     out["depth_controller"] = depth_controller_timing(T, stats, w)
     stats_np = T.read_turn_stats(stats)
-    del zs, zt, grad
+    del grad
+    torch.cuda.empty_cache()
+    out["topk"], topk_host = topk_timing(T, zs, zt, turn, traj, mask, w, args.steps, args.warmup)
+    del zs, zt
     torch.cuda.empty_cache()
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(w, args.cpu_sample_tokens)
         out["cpu_baseline"]["depth_controller_update_us"] = oracle_controller_timing(stats_np, w)
+        out["cpu_baseline"]["topk_tokens_per_s"] = oracle_topk_timing(w, topk_host)
     print(json.dumps(out), flush=True)
     return 0
 

@@ -66,6 +66,7 @@ typedef enum {
   TURNKL_ERR_PAD_MASK = -6,      /* device: padding token (traj_id < 0) with mask 1 */
   TURNKL_ERR_HIP = -7,           /* a HIP runtime call failed */
   TURNKL_ERR_SYNC_TIMEOUT = -8,  /* device: cross-workgroup exchange did not complete */
+  TURNKL_ERR_TOPK_ID = -9,       /* device: a top-K support id outside [0, vocab) */
 } turnkl_status;
 
 /* Statistics of one turn index t over the supervised tokens at that turn. */
@@ -197,6 +198,59 @@ int turnkl_profile_row_kernel(hipEvent_t before, hipEvent_t after);
  * outside 0..25.
  */
 int turnkl_set_row_tiling(int vectors_per_thread);
+
+/* ------------------------------------------------------------------------
+ * Top-K variant of the loss: the reverse KL on the teacher's top-K support
+ * (App. D: Algorithm 1 computes top-K reverse-KL token losses; the
+ * configuration table sets the teacher's top-K support size, K = 50).  The
+ * paper does not print the formula; this library renormalises both
+ * distributions on the support S_i of token i:
+ *   p^_s(v) = exp(a_v) / sum_{u in S_i} exp(a_u),  p^_t(v) likewise from the
+ *   teacher's values b_v on S_i (logits or log-probabilities: a per-row
+ *   constant cancels),
+ *   KL_i = sum_{v in S_i} p^_s(v) (log p^_s(v) - log p^_t(v))   (Sec. 3, Eq.
+ *   opd-rkl restricted to S_i),
+ *   G[i, v] = grad_scale * w_i * p^_s(v) (log p^_s(v) - log p^_t(v) - KL_i)
+ *   for v in S_i and 0 for every other id.
+ * Segments, weights, losses and per-turn statistics are those of
+ * turnkl_fwd_bwd, computed from these KL_i.
+ * ------------------------------------------------------------------------ */
+
+/* Workspace bytes for turnkl_fwd_bwd_topk (host); 0 for invalid arguments. */
+size_t turnkl_topk_workspace_bytes(int64_t n_tokens, int32_t k, int32_t max_turns);
+
+/*
+ * Top-K fused forward + backward.  Arguments as for turnkl_fwd_bwd, except:
+ *   teacher_ids    device, int32 [n_tokens][ld_topk]: row i holds the K
+ *                  distinct ids of S_i in [0, vocab) (a duplicate id counts
+ *                  twice and makes the dense gradient's entry unspecified);
+ *   teacher_vals   device, float32 [n_tokens][ld_topk]: the teacher's values
+ *                  at those ids;
+ *   k              1 .. min(1024, vocab);
+ *   grad_out       optional dense gradient, dtype [n_tokens][ld_grad], zero
+ *                  off the support; may equal student_logits with the same
+ *                  leading dimension (in place: every student logit is read
+ *                  before any gradient row is written);
+ *   grad_topk_out  optional, float32 [n_tokens][ld_grad_topk]: G on the
+ *                  support, in the order of teacher_ids (zeros for
+ *                  unsupervised tokens);
+ *   workspace      at least turnkl_topk_workspace_bytes(n_tokens, k, max_turns).
+ * Only the rows of supervised tokens are read from student_logits, teacher_ids
+ * and teacher_vals.  Errors: as turnkl_fwd_bwd (TURNKL_ERR_ALIAS when either
+ * gradient output overlaps an input or the other output), plus the device
+ * error TURNKL_ERR_TOPK_ID for an id outside [0, vocab) in a supervised row.
+ * The profiling hook of turnkl_profile_row_kernel brackets the two top-K
+ * kernels (support rows, then the dense zero-fill and scatter).
+ */
+int turnkl_fwd_bwd_topk(const void* student_logits, int64_t ld_student, int dtype,
+                        int64_t n_tokens, int64_t vocab, const int32_t* teacher_ids,
+                        const float* teacher_vals, int64_t ld_topk, int32_t k,
+                        const int32_t* turn_id, const int32_t* traj_id, const uint8_t* loss_mask,
+                        double alpha, float grad_scale, float* loss_out, void* grad_out,
+                        int64_t ld_grad, float* grad_topk_out, int64_t ld_grad_topk,
+                        turnkl_turn_stat* turn_stats_out, int32_t max_turns, int accumulate_stats,
+                        float* token_kl_out, void* workspace, size_t workspace_bytes,
+                        hipStream_t stream);
 
 /* ------------------------------------------------------------------------
  * Adaptive rollout-depth controller (Sec. 5.1; App. D, Algorithm 1 and the

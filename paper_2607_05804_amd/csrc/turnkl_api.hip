@@ -177,6 +177,98 @@ int turnkl_fwd_bwd(const void* student_logits, int64_t ld_student, const void* t
   return TURNKL_OK;
 }
 
+size_t turnkl_topk_workspace_bytes(int64_t n_tokens, int32_t k, int32_t max_turns) {
+  if (n_tokens < 0 || k < 1 || k > kMaxTopK || max_turns < 1) return 0;
+  return make_layout(n_tokens, 0, k).total;
+}
+
+int turnkl_fwd_bwd_topk(const void* student_logits, int64_t ld_student, int dtype,
+                        int64_t n_tokens, int64_t vocab, const int32_t* teacher_ids,
+                        const float* teacher_vals, int64_t ld_topk, int32_t k,
+                        const int32_t* turn_id, const int32_t* traj_id, const uint8_t* loss_mask,
+                        double alpha, float grad_scale, float* loss_out, void* grad_out,
+                        int64_t ld_grad, float* grad_topk_out, int64_t ld_grad_topk,
+                        turnkl_turn_stat* turn_stats_out, int32_t max_turns, int accumulate_stats,
+                        float* token_kl_out, void* workspace, size_t workspace_bytes,
+                        hipStream_t stream) {
+  // ---- arguments
+  if (dtype != TURNKL_BF16 && dtype != TURNKL_F32) return TURNKL_ERR_INVALID_ARG;
+  const size_t es = dtype == TURNKL_BF16 ? 2 : 4;
+  if (n_tokens < 0 || n_tokens > 0x7FFFFFFFll || vocab < 1 || max_turns < 1)
+    return TURNKL_ERR_INVALID_ARG;
+  if ((unsigned long long)vocab * es > 0x7FFFFFFFull) return TURNKL_ERR_INVALID_ARG;
+  if (k < 1 || k > kMaxTopK || k > vocab) return TURNKL_ERR_INVALID_ARG;
+  if (!(alpha >= 0.0 && alpha <= 1.0)) return TURNKL_ERR_INVALID_ARG;
+  if (!isfinite(grad_scale)) return TURNKL_ERR_INVALID_ARG;
+  if (!loss_out || !workspace) return TURNKL_ERR_INVALID_ARG;
+  if (n_tokens > 0) {
+    if (!student_logits || !teacher_ids || !teacher_vals || !turn_id || !traj_id || !loss_mask)
+      return TURNKL_ERR_INVALID_ARG;
+    if (ld_student < vocab || ld_topk < k) return TURNKL_ERR_INVALID_ARG;
+    if (grad_out && ld_grad < vocab) return TURNKL_ERR_INVALID_ARG;
+    if (grad_topk_out && ld_grad_topk < k) return TURNKL_ERR_INVALID_ARG;
+  }
+  if (((uintptr_t)workspace & 255u) != 0) return TURNKL_ERR_WORKSPACE;
+  if (n_tokens > 0) {
+    const size_t nid = matrix_bytes(n_tokens, ld_topk, k, 4);
+    if (grad_out) {
+      const size_t ng = matrix_bytes(n_tokens, ld_grad, vocab, es);
+      const size_t ns = matrix_bytes(n_tokens, ld_student, vocab, es);
+      if (overlaps(grad_out, ng, teacher_ids, nid) || overlaps(grad_out, ng, teacher_vals, nid))
+        return TURNKL_ERR_ALIAS;
+      const bool in_place = grad_out == student_logits && ld_grad == ld_student;
+      if (!in_place && overlaps(grad_out, ng, student_logits, ns)) return TURNKL_ERR_ALIAS;
+      if (grad_topk_out &&
+          overlaps(grad_out, ng, grad_topk_out, matrix_bytes(n_tokens, ld_grad_topk, k, 4)))
+        return TURNKL_ERR_ALIAS;
+    }
+    if (grad_topk_out) {
+      const size_t nt = matrix_bytes(n_tokens, ld_grad_topk, k, 4);
+      const size_t ns = matrix_bytes(n_tokens, ld_student, vocab, es);
+      if (overlaps(grad_topk_out, nt, teacher_ids, nid) || overlaps(grad_topk_out, nt, teacher_vals, nid) ||
+          overlaps(grad_topk_out, nt, student_logits, ns))
+        return TURNKL_ERR_ALIAS;
+    }
+  }
+  const Layout L = make_layout(n_tokens, 0, k);
+  if (workspace_bytes < L.total) return TURNKL_ERR_WORKSPACE;
+  const Ws ws = bind(workspace, L);
+  float* kl = token_kl_out ? token_kl_out : ws.kl;
+
+  // ---- launches
+  const SegParams sp{traj_id, turn_id, loss_mask, (long long)n_tokens, max_turns};
+  if (launch_segments(sp, ws, L.nblk, stream) != hipSuccess) return TURNKL_ERR_HIP;
+  if (launch_weights(sp, ws, alpha, grad_scale, 0, kl, stream) != hipSuccess) return TURNKL_ERR_HIP;
+  TopkParams tp{};
+  tp.zs = student_logits;
+  tp.ids = teacher_ids;
+  tp.vals = teacher_vals;
+  tp.stage = grad_topk_out ? grad_topk_out : ws.topk;
+  tp.grad = grad_out;
+  tp.mask = loss_mask;
+  tp.wsc = ws.wsc;
+  tp.kl = kl;
+  tp.hdr = ws.hdr;
+  tp.ld_s = ld_student;
+  tp.ld_k = ld_topk;
+  tp.ld_stage = grad_topk_out ? ld_grad_topk : k;
+  tp.ld_g = grad_out ? ld_grad : 0;
+  tp.n_rows = (int)n_tokens;
+  tp.vocab = (int)vocab;
+  tp.k = k;
+  tp.bf16 = dtype == TURNKL_BF16;
+  tp.zero_masked_stage = grad_topk_out != nullptr;
+  const bool prof = t_row_before && t_row_after;
+  if (prof && hipEventRecord(t_row_before, stream) != hipSuccess) return TURNKL_ERR_HIP;
+  if (launch_topk_rows(tp, stream) != hipSuccess) return TURNKL_ERR_HIP;
+  if (launch_topk_dense(tp, stream) != hipSuccess) return TURNKL_ERR_HIP;
+  if (prof && hipEventRecord(t_row_after, stream) != hipSuccess) return TURNKL_ERR_HIP;
+  if (launch_reduce(sp, ws, kl, alpha, loss_out, turn_stats_out, accumulate_stats, stream) !=
+      hipSuccess)
+    return TURNKL_ERR_HIP;
+  return TURNKL_OK;
+}
+
 int turnkl_get_status(const void* workspace, hipStream_t stream) {
   if (!workspace) return TURNKL_ERR_INVALID_ARG;
   const Header* hdr = static_cast<const Header*>(workspace);
@@ -230,6 +322,7 @@ const char* turnkl_status_string(int status) {
     case TURNKL_ERR_PAD_MASK: return "padding token with loss mask set";
     case TURNKL_ERR_HIP: return "HIP runtime error";
     case TURNKL_ERR_SYNC_TIMEOUT: return "row exchange timed out";
+    case TURNKL_ERR_TOPK_ID: return "top-K support id outside [0, vocab)";
     default: return "unknown status";
   }
 }

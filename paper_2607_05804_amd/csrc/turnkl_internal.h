@@ -14,7 +14,13 @@ namespace turnkl {
 // error, then a turn-range error, then an ordering error.
 
 constexpr unsigned long long kNoError = ~0ull;
-enum : unsigned { kPrioPadMask = 0, kPrioTurnRange = 1, kPrioUnsorted = 2, kPrioTimeout = 3 };
+enum : unsigned {
+  kPrioPadMask = 0,
+  kPrioTurnRange = 1,
+  kPrioUnsorted = 2,
+  kPrioTimeout = 3,
+  kPrioTopkId = 4,  // top-K path: a support id outside [0, vocab)
+};
 
 __host__ __device__ inline unsigned long long err_key(long long pos, unsigned prio) {
   return ((unsigned long long)pos << 4) | prio;
@@ -26,6 +32,7 @@ inline int status_from_key(unsigned long long key) {
     case kPrioPadMask: return TURNKL_ERR_PAD_MASK;
     case kPrioTurnRange: return TURNKL_ERR_TURN_RANGE;
     case kPrioUnsorted: return TURNKL_ERR_UNSORTED;
+    case kPrioTopkId: return TURNKL_ERR_TOPK_ID;
     default: return TURNKL_ERR_SYNC_TIMEOUT;
   }
 }
@@ -62,7 +69,7 @@ constexpr int kSegTile = kSegThreads * kSegTokensPerThread;
 // that).
 struct Layout {
   size_t header, blk_cnt, blk_off, blk_err, tok_seg, seg_start, seg_len, seg_traj, seg_turn,
-      seg_nsup, seg_head, traj_T, traj_N, w, wsc, kl, seg_stat, slots, total;
+      seg_nsup, seg_head, traj_T, traj_N, w, wsc, kl, seg_stat, slots, topk, total;
   long long nblk;
   int n_chunks;
 };
@@ -72,7 +79,9 @@ inline size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
 // 64-bit words a row-kernel chunk publishes to its row mates
 constexpr int kExchangeWords = 7;
 
-inline Layout make_layout(long long n_tokens, int n_chunks) {
+// n_chunks > 1: exchange slots of the full-vocabulary row kernel; topk_k > 0:
+// the top-K path's staging of the scaled gradient on each row's support.
+inline Layout make_layout(long long n_tokens, int n_chunks, int topk_k = 0) {
   Layout L{};
   const size_t n = (size_t)n_tokens;
   L.nblk = (n_tokens + kSegTile - 1) / kSegTile;
@@ -97,6 +106,7 @@ inline Layout make_layout(long long n_tokens, int n_chunks) {
   L.kl = take(n * 4);
   L.seg_stat = take(n * sizeof(SegStat));
   L.slots = take(n * (size_t)n_chunks * kExchangeWords * 8);
+  L.topk = take(n * (size_t)topk_k * 4);
   L.total = o;
   return L;
 }
@@ -121,6 +131,7 @@ struct Ws {
   float* kl;
   SegStat* seg_stat;
   unsigned long long* slots;
+  float* topk;
 };
 
 inline Ws bind(void* base, const Layout& L) {
@@ -144,6 +155,7 @@ inline Ws bind(void* base, const Layout& L) {
   w.kl = reinterpret_cast<float*>(b + L.kl);
   w.seg_stat = reinterpret_cast<SegStat*>(b + L.seg_stat);
   w.slots = reinterpret_cast<unsigned long long*>(b + L.slots);
+  w.topk = reinterpret_cast<float*>(b + L.topk);
   return w;
 }
 
@@ -205,6 +217,36 @@ struct RowParams {
 };
 
 hipError_t launch_rows(const RowParams& p, const RowTiling& t, hipStream_t s);
+
+// Top-K path (the teacher's top-K support; both distributions renormalised on
+// it).  The row kernel writes each supervised row's scaled gradient on the
+// support to `stage` (row stride ld_stage) and its KL; the dense kernel then
+// zero-fills every gradient row and scatters the staged values into it.
+struct TopkParams {
+  const void* zs;
+  const int* ids;
+  const float* vals;
+  float* stage;
+  void* grad;
+  const unsigned char* mask;
+  const float* wsc;
+  float* kl;
+  Header* hdr;
+  long long ld_s;
+  long long ld_k;      // row stride of ids and vals
+  long long ld_stage;  // row stride of stage
+  long long ld_g;
+  int n_rows;
+  int vocab;
+  int k;
+  int bf16;
+  int zero_masked_stage;  // write zeros to stage rows of unsupervised tokens
+};
+
+constexpr int kMaxTopK = 1024;
+
+hipError_t launch_topk_rows(const TopkParams& p, hipStream_t s);
+hipError_t launch_topk_dense(const TopkParams& p, hipStream_t s);
 
 hipError_t launch_reduce(const SegParams& p, const Ws& ws, const float* kl, double alpha,
                          float* loss_out, turnkl_turn_stat* stats, int accumulate,

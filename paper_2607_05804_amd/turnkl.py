@@ -25,6 +25,7 @@ ERR_TURN_RANGE = -5
 ERR_PAD_MASK = -6
 ERR_HIP = -7
 ERR_SYNC_TIMEOUT = -8
+ERR_TOPK_ID = -9
 
 BF16 = 0
 F32 = 1
@@ -33,6 +34,7 @@ F32 = 1
 EXPORTS = ("turnkl_workspace_bytes", "turnkl_fwd_bwd", "turnkl_get_status",
            "turnkl_get_segments", "turnkl_alpha_schedule", "turnkl_status_string",
            "turnkl_profile_row_kernel", "turnkl_set_row_tiling",
+           "turnkl_topk_workspace_bytes", "turnkl_fwd_bwd_topk",
            "turnkl_depth_default_config", "turnkl_depth_init", "turnkl_depth_plan",
            "turnkl_depth_update")
 
@@ -93,6 +95,14 @@ def lib() -> ctypes.CDLL:
         l.turnkl_profile_row_kernel.argtypes = [c.c_void_p, c.c_void_p]
         l.turnkl_set_row_tiling.restype = c.c_int
         l.turnkl_set_row_tiling.argtypes = [c.c_int]
+        l.turnkl_topk_workspace_bytes.restype = c.c_size_t
+        l.turnkl_topk_workspace_bytes.argtypes = [c.c_int64, c.c_int32, c.c_int32]
+        l.turnkl_fwd_bwd_topk.restype = c.c_int
+        l.turnkl_fwd_bwd_topk.argtypes = [
+            c.c_void_p, c.c_int64, c.c_int, c.c_int64, c.c_int64, c.c_void_p, c.c_void_p,
+            c.c_int64, c.c_int32, c.c_void_p, c.c_void_p, c.c_void_p, c.c_double, c.c_float,
+            c.c_void_p, c.c_void_p, c.c_int64, c.c_void_p, c.c_int64, c.c_void_p, c.c_int32,
+            c.c_int, c.c_void_p, c.c_void_p, c.c_size_t, c.c_void_p]
         l.turnkl_depth_default_config.restype = None
         l.turnkl_depth_default_config.argtypes = [c.POINTER(DepthConfig)]
         l.turnkl_depth_init.restype = c.c_int
@@ -236,6 +246,87 @@ def fwd_bwd(student: torch.Tensor, teacher: torch.Tensor, turn_id: torch.Tensor,
         if st != OK:
             raise TurnKLError(st, "turnkl_fwd_bwd (device)")
     return loss, grad_t, turn_stats, kl_t, workspace
+
+
+class TopkWorkspace(Workspace):
+    """Caller-owned device scratch for turnkl_fwd_bwd_topk."""
+
+    def __init__(self, n_tokens: int, k: int, max_turns: int, device="cuda"):
+        nbytes = int(lib().turnkl_topk_workspace_bytes(n_tokens, k, max_turns))
+        if nbytes == 0:
+            raise TurnKLError(ERR_INVALID_ARG, "turnkl_topk_workspace_bytes")
+        self.tensor = torch.empty(nbytes, dtype=torch.uint8, device=device)
+        self.nbytes = nbytes
+        self.n_tokens = n_tokens
+
+
+def fwd_bwd_topk(student: torch.Tensor, teacher_ids: torch.Tensor, teacher_vals: torch.Tensor,
+                 turn_id: torch.Tensor, traj_id: torch.Tensor, loss_mask: torch.Tensor,
+                 alpha: float, *, grad_scale: float = 1.0,
+                 grad: str | torch.Tensor | None = "new", grad_topk: bool | torch.Tensor = False,
+                 max_turns: int = 64, turn_stats: torch.Tensor | None = None,
+                 accumulate_stats: bool = False, token_kl: bool | torch.Tensor = False,
+                 workspace: TopkWorkspace | None = None, check: bool = True):
+    """The top-K variant (turnkl_fwd_bwd_topk) on the current stream.
+
+    teacher_ids: int32 [N, K]; teacher_vals: float32 [N, K].  grad as in
+    fwd_bwd (dense, zero off the support); grad_topk: True allocates, or a
+    float32 [N, K] tensor receives, the gradient on the support.  Returns
+    (loss[3], grad or None, grad_topk or None, turn_stats or None,
+    token_kl or None, workspace).
+    """
+    dt = _dtype_code(student)
+    n, v = (int(student.shape[0]), int(student.shape[1])) if student.dim() == 2 else (0, 0)
+    if teacher_ids.dtype != torch.int32 or teacher_vals.dtype != torch.float32:
+        raise TypeError("teacher_ids must be int32 and teacher_vals float32")
+    if teacher_ids.dim() != 2 or teacher_ids.shape != teacher_vals.shape or teacher_ids.shape[0] != n:
+        raise ValueError("teacher_ids / teacher_vals must both be [n_tokens, K]")
+    if teacher_ids.stride() != teacher_vals.stride():
+        raise ValueError("teacher_ids and teacher_vals must share a row stride")
+    k = int(teacher_ids.shape[1])
+    for t in (turn_id, traj_id):
+        if t.dtype != torch.int32 or t.numel() != n:
+            raise ValueError("turn_id / traj_id must be int32 with one entry per row")
+    if loss_mask.dtype != torch.uint8 or loss_mask.numel() != n:
+        raise ValueError("loss_mask must be uint8 with one entry per row")
+    dev = student.device
+    if isinstance(grad, str):
+        if grad == "new":
+            grad_t = torch.empty_like(student)
+        elif grad == "inplace":
+            grad_t = student
+        else:
+            raise ValueError(grad)
+    else:
+        grad_t = grad
+    if isinstance(grad_topk, torch.Tensor):
+        gk = grad_topk
+    else:
+        gk = torch.empty((max(n, 1), k), dtype=torch.float32, device=dev) if grad_topk else None
+    if workspace is None:
+        workspace = TopkWorkspace(n, k, max_turns, device=dev)
+    loss = torch.empty(3, dtype=torch.float32, device=dev)
+    if isinstance(token_kl, torch.Tensor):
+        kl_t = token_kl
+    else:
+        kl_t = torch.empty(max(n, 1), dtype=torch.float32, device=dev) if token_kl else None
+    stream = torch.cuda.current_stream(dev).cuda_stream
+    ld_k = int(teacher_ids.stride(0)) if n else k
+    rc = lib().turnkl_fwd_bwd_topk(
+        _ptr(student), _row_stride(student) if n else v, dt, n, v, _ptr(teacher_ids),
+        _ptr(teacher_vals), ld_k, k, _ptr(turn_id), _ptr(traj_id), _ptr(loss_mask), float(alpha),
+        float(grad_scale), _ptr(loss), _ptr(grad_t),
+        (_row_stride(grad_t) if n else v) if grad_t is not None else 0, _ptr(gk),
+        (int(gk.stride(0)) if n else k) if gk is not None else 0, _ptr(turn_stats),
+        int(max_turns), int(bool(accumulate_stats)), _ptr(kl_t), _ptr(workspace.tensor),
+        workspace.nbytes, ctypes.c_void_p(stream))
+    if rc != OK:
+        raise TurnKLError(rc, "turnkl_fwd_bwd_topk")
+    if check:
+        st = workspace.status()
+        if st != OK:
+            raise TurnKLError(st, "turnkl_fwd_bwd_topk (device)")
+    return loss, grad_t, gk, turn_stats, kl_t, workspace
 
 
 def new_turn_stats(max_turns: int, device="cuda") -> torch.Tensor:

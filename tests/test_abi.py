@@ -122,3 +122,54 @@ def test_binding_fails_loudly_without_library(monkeypatch, tmp_path):
     monkeypatch.setattr(T, "LIB_PATH", str(tmp_path / "missing.so"))
     with pytest.raises(RuntimeError, match="not built"):
         T.lib()
+
+
+def _call_topk(**kw):
+    """turnkl_fwd_bwd_topk with fake (never dereferenced) addresses."""
+    n, v, k = kw.get("n", 64), kw.get("v", 1024), kw.get("k", 50)
+    ws_bytes = T.lib().turnkl_topk_workspace_bytes(n, k, kw.get("max_turns", 8))
+    args = dict(zs=0x100000000, ld_s=v, dtype=T.BF16, n=n, v=v, ids=0x200000000,
+                vals=0x210000000, ld_k=k, k=k, turn=0x300000000, traj=0x300100000,
+                mask=0x300200000, alpha=0.5, scale=1.0, loss=0x300300000, grad=0x400000000,
+                ld_g=v, gk=0x600000000, ld_gk=k, stats=0, max_turns=8, acc=0, kl=0,
+                ws=0x500000000, ws_bytes=ws_bytes)
+    args.update(kw)
+    p = lambda x: ctypes.c_void_p(x) if x else None
+    return T.lib().turnkl_fwd_bwd_topk(
+        p(args["zs"]), args["ld_s"], args["dtype"], args["n"], args["v"], p(args["ids"]),
+        p(args["vals"]), args["ld_k"], args["k"], p(args["turn"]), p(args["traj"]), p(args["mask"]),
+        args["alpha"], args["scale"], p(args["loss"]), p(args["grad"]), args["ld_g"], p(args["gk"]),
+        args["ld_gk"], p(args["stats"]), args["max_turns"], args["acc"], p(args["kl"]),
+        p(args["ws"]), args["ws_bytes"], None)
+
+
+def test_topk_workspace_bytes():
+    a = T.lib().turnkl_topk_workspace_bytes(1000, 50, 8)
+    b = T.lib().turnkl_topk_workspace_bytes(1000, 100, 8)
+    assert 0 < a < b and a % 256 == 0
+    assert T.lib().turnkl_topk_workspace_bytes(1000, 0, 8) == 0
+    assert T.lib().turnkl_topk_workspace_bytes(1000, 1025, 8) == 0
+    assert T.lib().turnkl_topk_workspace_bytes(-1, 50, 8) == 0
+
+
+@pytest.mark.parametrize("kw,code", [
+    (dict(dtype=3), T.ERR_INVALID_ARG),
+    (dict(k=0), T.ERR_INVALID_ARG),
+    (dict(k=1025, ld_k=1025, ld_gk=1025), T.ERR_INVALID_ARG),
+    (dict(k=64, v=32, ld_s=32, ld_g=32, ld_k=64, ld_gk=64), T.ERR_INVALID_ARG),  # K > V
+    (dict(ld_k=49), T.ERR_INVALID_ARG),
+    (dict(ld_gk=10), T.ERR_INVALID_ARG),
+    (dict(ld_s=1000), T.ERR_INVALID_ARG),
+    (dict(ids=0), T.ERR_INVALID_ARG),
+    (dict(vals=0), T.ERR_INVALID_ARG),
+    (dict(alpha=2.0), T.ERR_INVALID_ARG),
+    # outputs overlapping inputs or each other (exact in-place dense is allowed)
+    (dict(grad=0x200000000), T.ERR_ALIAS),
+    (dict(grad=0x100000000 + 2), T.ERR_ALIAS),
+    (dict(gk=0x210000000), T.ERR_ALIAS),
+    (dict(gk=0x100000000), T.ERR_ALIAS),
+    (dict(gk=0x400000000 + 4096), T.ERR_ALIAS),
+    (dict(ws_bytes=1024), T.ERR_WORKSPACE),
+])
+def test_topk_host_rejects_bad_arguments_before_launch(kw, code):
+    assert _call_topk(**kw) == code

@@ -1,0 +1,173 @@
+"""Parity of the top-K path (turnkl_fwd_bwd_topk) with the top-K oracle:
+loss, per-token KL, per-turn statistics, the gradient on the support (sparse
+output) and the dense gradient (support values, zeros elsewhere)."""
+import numpy as np
+import pytest
+import torch
+
+import synth
+from gpu_support import (check_loss, check_segments, check_stats, check_token_kl, ids_to_device,
+                         log, rows_to_host, sample_rows, to_device_logits)
+from oracle import topk_oracle as K
+from oracle import turnkl_oracle as O
+from paper_2607_05804_amd import turnkl as T
+from test_gpu_edges import make_batch
+
+pytestmark = pytest.mark.gpu
+
+
+def _support(zt_f32: np.ndarray, k: int, rng=None):
+    """The teacher's top-k ids per row (ties broken by id) and its values there."""
+    order = np.argsort(-zt_f32, axis=1, kind="stable")[:, :k]
+    if rng is not None:  # the order inside the support carries no meaning
+        order = np.take_along_axis(order, np.argsort(rng.random(order.shape), axis=1), axis=1)
+    vals = np.take_along_axis(zt_f32, order, axis=1)
+    return order.astype(np.int32), vals.astype(np.float32)
+
+
+def _f32(h):
+    return (h.astype(np.uint32) << 16).view(np.float32) if h.dtype == np.uint16 else h
+
+
+def check_topk_grads(gk_dev, dense_dev, ref, ids, w_scale, rows, mask, bf16_dense):
+    """Unweighted comparison g_hat = G / (grad_scale w_i) against the oracle."""
+    gk = gk_dev.cpu().numpy().astype(np.float64) if gk_dev is not None else None
+    D = rows_to_host(dense_dev, rows).astype(np.float64) if dense_dev is not None else None
+    for k_, r in enumerate(rows):
+        if not mask[r]:
+            if gk is not None:
+                assert np.all(gk[r] == 0.0)
+            if D is not None:
+                assert np.all(D[k_] == 0.0)
+            continue
+        g = ref.grads[r]
+        scale = w_scale * ref.w[r]
+        if gk is not None:
+            err = np.abs(gk[r] / scale - g)
+            assert np.all(err <= 1e-4 * np.abs(g) + 2e-6), (r, err.max())
+        if D is not None:
+            row = D[k_]
+            got = row[ids[r]] / scale
+            err = np.abs(got - g)
+            bound = (2.0 ** -8 * np.abs(g) + 2e-5) if bf16_dense else (1e-4 * np.abs(g) + 2e-6)
+            assert np.all(err <= bound), (r, err.max())
+            off = np.ones(row.shape[0], bool)
+            off[ids[r]] = False
+            assert np.all(row[off] == 0.0)
+
+
+def _run(zs_h, ids, vals, traj, turn, mask, alpha=0.4, max_turns=8, grad_scale=1.0,
+         grad="new", grad_topk=True):
+    zs = to_device_logits(zs_h)
+    turn_d, traj_d, mask_d = ids_to_device(traj, turn, mask)
+    stats = T.new_turn_stats(max_turns)
+    out = T.fwd_bwd_topk(zs, torch.from_numpy(ids).cuda(), torch.from_numpy(vals).cuda(), turn_d,
+                         traj_d, mask_d, alpha, grad_scale=grad_scale, grad=grad,
+                         grad_topk=grad_topk, max_turns=max_turns, turn_stats=stats, token_kl=True)
+    torch.cuda.synchronize()
+    dt = O.DTYPE_BF16 if zs_h.dtype == np.uint16 else O.DTYPE_F32
+    ref = K.fwd_bwd_topk(traj, turn, mask, alpha, max_turns,
+                         lambda rows, i: np.take_along_axis(zs_h[rows], i, axis=1), ids, vals, dt,
+                         grad_scale)
+    return out, ref, zs
+
+
+@pytest.mark.parametrize("V,dtype,k", [(32000, "bf16", 50), (32000, "bf16", 1), (4096, "bf16", 64),
+                                       (4096, "bf16", 65), (5000, "f32", 100), (2048, "bf16", 1024),
+                                       (1001, "bf16", 50), (1000, "f32", 7)])
+def test_topk_parity(V, dtype, k, gpu):
+    log(f"topk V={V} {dtype} K={k}")
+    traj, turn, mask, zs_h, zt_h = make_batch(60 + k, V=V, dtype=dtype)
+    rng = np.random.default_rng(k)
+    ids, vals = _support(_f32(zt_h), k, rng)
+    (loss, g, gk, stats, kl, ws), ref, _ = _run(zs_h, ids, vals, traj, turn, mask)
+    check_segments(ws, ref.seg)
+    check_loss(loss, ref.loss)
+    check_token_kl(kl, ref.kl, mask)
+    check_stats(stats, ref.stats)
+    rows = list(range(len(traj)))
+    check_topk_grads(gk, g, ref, ids, 1.0, rows, mask, dtype == "bf16")
+
+
+def test_topk_in_place_forward_only_and_scale(gpu):
+    traj, turn, mask, zs_h, zt_h = make_batch(71, V=8192, dtype="bf16")
+    ids, vals = _support(_f32(zt_h), 50)
+    (l1, g1, gk1, _, k1, _), ref, _ = _run(zs_h, ids, vals, traj, turn, mask, grad_scale=-0.75)
+    (l2, g2, gk2, _, k2, _), _, zs2 = _run(zs_h, ids, vals, traj, turn, mask, grad_scale=-0.75,
+                                           grad="inplace")
+    assert g2.data_ptr() == zs2.data_ptr()
+    assert torch.equal(g1.view(torch.int16), g2.view(torch.int16))
+    assert torch.equal(gk1, gk2) and torch.equal(l1, l2) and torch.equal(k1, k2)
+    check_topk_grads(gk1, g1, ref, ids, -0.75, list(range(len(traj))), mask, True)
+    (l3, g3, gk3, _, k3, _), _, _ = _run(zs_h, ids, vals, traj, turn, mask, grad=None,
+                                         grad_topk=False)
+    assert g3 is None and gk3 is None
+    assert torch.equal(l3, l1) and torch.equal(k3, k1)
+
+
+def test_topk_identical_values_give_exact_zeros(gpu):
+    traj, turn, mask, zs_h, _ = make_batch(72, V=4096, dtype="bf16")
+    ids, _ = _support(_f32(zs_h), 50)
+    vals = np.take_along_axis(_f32(zs_h), ids.astype(np.int64), axis=1).astype(np.float32)
+    (loss, g, gk, _, kl, _), _, _ = _run(zs_h, ids, vals, traj, turn, mask)
+    assert torch.count_nonzero(loss).item() == 0
+    assert torch.count_nonzero(kl).item() == 0
+    assert torch.count_nonzero(gk).item() == 0
+    assert torch.count_nonzero(g.float()).item() == 0
+
+
+def test_topk_bad_id_is_a_device_error(gpu):
+    traj, turn, mask, zs_h, zt_h = make_batch(73, V=2048, dtype="bf16", pad=False)
+    ids, vals = _support(_f32(zt_h), 16)
+    r = int(np.nonzero(mask)[0][3])
+    ids = ids.copy()
+    ids[r, 5] = 2048
+    zs = to_device_logits(zs_h)
+    turn_d, traj_d, mask_d = ids_to_device(traj, turn, mask)
+    with pytest.raises(T.TurnKLError) as e:
+        T.fwd_bwd_topk(zs, torch.from_numpy(ids).cuda(), torch.from_numpy(vals).cuda(), turn_d,
+                       traj_d, mask_d, 0.5, max_turns=8)
+    assert e.value.code == T.ERR_TOPK_ID
+    # an out-of-range id in an unsupervised row is never read
+    u = int(np.nonzero(mask == 0)[0][0])
+    ids2, _ = _support(_f32(zt_h), 16)
+    ids2[u, 0] = -7
+    T.fwd_bwd_topk(zs, torch.from_numpy(ids2).cuda(), torch.from_numpy(vals).cuda(), turn_d,
+                   traj_d, mask_d, 0.5, max_turns=8)
+    torch.cuda.synchronize()
+
+
+def test_topk_full_size_long_horizon(gpu):
+    """65,536 tokens x V = 151,936 bf16, the teacher's top-50 from the
+    device-generated teacher logits; loss, KL and stats over every row, the
+    gradient on sampled rows."""
+    w = synth.make("long_horizon")
+    zs, zt = w.device_logits()
+    top_v, top_i = torch.topk(zt, 50, dim=1)  # bf16 values are exact in fp32
+    ids = top_i.to(torch.int32).contiguous()
+    vals = top_v.float().contiguous()
+    del zt
+    torch.cuda.empty_cache()
+    ids_h = ids.cpu().numpy()
+    vals_h = vals.cpu().numpy()
+    idx = torch.from_numpy(ids_h.astype(np.int64)).cuda()
+    zs_at = torch.gather(zs, 1, idx).contiguous().view(torch.int16).cpu().numpy().view(np.uint16)
+    del idx
+    rows = sample_rows(w.loss_mask, 24, 4, seed=2)
+    ref = K.fwd_bwd_topk(w.traj_id, w.turn_id, w.loss_mask, 0.5, w.max_turns,
+                         lambda r, i: zs_at[r], ids_h, vals_h, O.DTYPE_BF16)
+    log(f"  topk oracle done: loss={ref.loss}")
+    turn, traj, mask = ids_to_device(w.traj_id, w.turn_id, w.loss_mask)
+    stats = T.new_turn_stats(w.max_turns)
+    loss, g, gk, _, kl, ws = T.fwd_bwd_topk(zs, ids, vals, turn, traj, mask, 0.5, grad="inplace",
+                                            grad_topk=True, max_turns=w.max_turns,
+                                            turn_stats=stats, token_kl=True)
+    torch.cuda.synchronize()
+    check_segments(ws, ref.seg)
+    check_loss(loss, ref.loss)
+    check_token_kl(kl, ref.kl, w.loss_mask)
+    check_stats(stats, ref.stats)
+    check_topk_grads(gk, g, ref, ids_h, 1.0, rows, w.loss_mask, True)
+    log(f"  loss gpu={loss.tolist()} ref={ref.loss}")
+    del zs, g
+    torch.cuda.empty_cache()
