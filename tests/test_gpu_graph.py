@@ -1,0 +1,56 @@
+"""The fused call captured in a HIP graph: every replay equals the eager
+call bit for bit (the library enqueues only kernels, allocates nothing and
+never synchronises on the success path, and resets its ticket and exchange
+state with kernels, so a captured call can be replayed)."""
+import numpy as np
+import pytest
+import torch
+
+import synth
+from gpu_support import ids_to_device, log, to_device_logits
+from paper_2607_05804_amd import turnkl as T
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.mark.parametrize("vpt", [0, 4])
+def test_graph_replays_equal_eager(vpt, gpu):
+    w = synth.make("agent")
+    zs_h, zt_h = w.host_logits(0, w.n_tokens)
+    zs, zt = to_device_logits(zs_h), to_device_logits(zt_h)
+    turn, traj, mask = ids_to_device(w.traj_id, w.turn_id, w.loss_mask)
+    n, V = zs.shape
+    T.set_row_tiling(vpt)
+    try:
+        ws = T.Workspace(n, V, T.BF16, w.max_turns)
+        grad = torch.empty_like(zs)
+        kl = torch.empty(n, dtype=torch.float32, device=gpu)
+        stats = T.new_turn_stats(w.max_turns)
+        s = torch.cuda.Stream()
+        s.wait_stream(torch.cuda.current_stream())
+        with torch.cuda.stream(s):
+            # eager reference on the side stream
+            loss, _, _, _, _ = T.fwd_bwd(zs, zt, turn, traj, mask, 0.3, grad=grad,
+                                         max_turns=w.max_turns, turn_stats=stats, token_kl=kl,
+                                         workspace=ws, check=False)
+            s.synchronize()
+            ref = (loss.clone(), grad.clone(), kl.clone(), stats.clone())
+            g = torch.cuda.CUDAGraph()
+            with torch.cuda.graph(g, stream=s):
+                loss_g, _, _, _, _ = T.fwd_bwd(zs, zt, turn, traj, mask, 0.3, grad=grad,
+                                               max_turns=w.max_turns, turn_stats=stats,
+                                               token_kl=kl, workspace=ws, check=False)
+        torch.cuda.current_stream().wait_stream(s)
+        for r in range(4):
+            grad.fill_(7)  # eager work between replays
+            kl.zero_()
+            g.replay()
+            torch.cuda.synchronize()
+            assert ws.status() == T.OK
+            assert torch.equal(loss_g, ref[0]), r
+            assert torch.equal(grad.view(torch.int16), ref[1].view(torch.int16)), r
+            assert torch.equal(kl, ref[2]), r
+            assert torch.equal(stats, ref[3]), r
+        log(f"graph replays ok (vpt={vpt}): loss={loss_g.tolist()}")
+    finally:
+        T.set_row_tiling(0)
