@@ -61,23 +61,25 @@ def widen(values: np.ndarray, dtype: int) -> np.ndarray:
 
 def fwd_bwd_topk(traj_id, turn_id, loss_mask, alpha: float, max_turns: int, student_at,
                  teacher_ids: np.ndarray, teacher_vals: np.ndarray, dtype: int,
-                 grad_scale: float = 1.0, chunk_rows: int = 4096) -> O.Result:
+                 grad_scale: float = 1.0, chunk_rows: int = 4096, support_floor: int = 0,
+                 support_frac: float = 0.0, success=None) -> O.Result:
     """Reference for one call of the top-K path.
 
     student_at(rows, ids) -> student logits [len(rows), K] at those ids (in
     the storage dtype); teacher_ids, teacher_vals: [N, K] (int, float).  The
     returned Result's grads map each supervised row to its unweighted
-    gradient on the support, ordered as teacher_ids[row]."""
+    gradient on the support, ordered as teacher_ids[row].  support_floor,
+    support_frac and success act as in the full-vocabulary oracle."""
     traj_id = np.asarray(traj_id)
     loss_mask = np.asarray(loss_mask)
     n = int(traj_id.shape[0])
-    seg = O.segments(traj_id, turn_id, loss_mask, max_turns)
+    seg = O.segments(traj_id, turn_id, loss_mask, max_turns, success)
     if seg.status != O.OK:
         return O.Result(seg.status, seg, np.zeros(n), np.zeros(n), (np.nan,) * 3,
                         np.zeros(max_turns, O.STAT_DTYPE), {})
-    w = O.token_weights(seg, n, loss_mask, alpha)
-    w0 = O.token_weights(seg, n, loss_mask, 0.0)
-    w1 = O.token_weights(seg, n, loss_mask, 1.0)
+    w = O.token_weights(seg, n, loss_mask, alpha, support_floor, support_frac)
+    w0 = O.token_weights(seg, n, loss_mask, 0.0, support_floor, support_frac)
+    w1 = O.token_weights(seg, n, loss_mask, 1.0, support_floor, support_frac)
     kl = np.zeros(n, np.float64)
     grads = {}
     sup = np.nonzero(loss_mask)[0]
@@ -91,4 +93,5 @@ def fwd_bwd_topk(traj_id, turn_id, loss_mask, alpha: float, max_turns: int, stud
         for j, r in enumerate(rows.tolist()):
             grads[r] = g[j]
     stats = O.turn_stats([(seg, loss_mask, kl, w)], max_turns)
-    return O.Result(O.OK, seg, w, kl, O.losses(w, w0, w1, kl), stats, grads)
+    return O.Result(O.OK, seg, w, kl, O.losses(w, w0, w1, kl), stats, grads,
+                    O.outcome_split(seg, loss_mask, kl, w, max_turns))

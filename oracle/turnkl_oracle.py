@@ -26,6 +26,12 @@ It is a plain, slow, float64 statement of what the hot path computes:
                K_t drive the depth controller; Sec. 4.4: s_t, the turn's share
                of the loss mass.
   alpha_schedule  Sec. 5.2 / Algorithm 1: alpha = clip((k/K - s)/(e - s), 0, 1).
+  support floor   App. D (full-configuration table, internal blend): the
+               turn-level floor n_min = max(floor, ceil(frac * n_traj)), with
+               floor 8 and frac 0.15 in the paper; Sec. 7.2 calls the turns it
+               admits "valid turns" (turns reached by enough trajectories).
+  outcome split   Sec. 4.2: K_t^fail and K_t^succ, the per-turn KL means over
+               failed and successful rollouts, whose difference is G_t.
 
 Readings where the paper is silent (each is listed in the design doc):
   * the loss is over the full vocabulary (the paper trains a top-50 variant);
@@ -37,12 +43,27 @@ Readings where the paper is silent (each is listed in the design doc):
     one segment to the next, turn ids increase within a trajectory, and
     0 <= turn id < max_turns; the first violation in token order is reported;
   * per-turn variance is the population variance (ddof = 0);
-  * no clamp is applied to per-token KL.
+  * no clamp is applied to per-token KL;
+  * support floor (the paper does not say how n_min enters the turn term):
+    n_traj is B, the trajectories of the call with a supervised token; turn t
+    is valid when its survivor count n_t (trajectories with a supervised token
+    at t) is at least n_min, with frac * B rounded once in float64 before the
+    ceiling; a trajectory's turn term gives each of its valid supervised turns
+    1 / T_v (T_v of them) and its other turns 0; a trajectory with no valid
+    supervised turn takes its trajectory term for the turn term.  floor = 0
+    and frac = 0 admit every supervised turn (the plain blend);
+  * outcome flags are per token, equal across every non-padding token of a
+    trajectory (padding tokens' flags are ignored); nonzero means success.
+    The first token in token order where a flag differs from the one before
+    it in its segment, or a segment start whose flag differs from its
+    trajectory's first segment, is an error (after the other checks at the
+    same token).
 """
 from __future__ import annotations
 
 import ctypes
 import dataclasses
+import math
 import os
 
 import numpy as np
@@ -54,6 +75,7 @@ OK = 0
 ERR_UNSORTED = -4
 ERR_TURN_RANGE = -5
 ERR_PAD_MASK = -6
+ERR_OUTCOME = -10
 
 DTYPE_BF16 = 0
 DTYPE_F32 = 1
@@ -96,18 +118,24 @@ class Segments:
     traj: np.ndarray    # trajectory id
     turn: np.ndarray    # turn id
     n_sup: np.ndarray   # supervised tokens, n_t for (traj, turn)
+    success: np.ndarray = None  # outcome flag (0/1) of the segment's trajectory, if given
 
     @property
     def count(self) -> int:
         return int(self.start.shape[0])
 
 
-def segments(traj_id, turn_id, loss_mask, max_turns: int) -> Segments:
-    """Walk the packed tokens in order and cut them into (trajectory, turn) runs."""
+def segments(traj_id, turn_id, loss_mask, max_turns: int, success=None) -> Segments:
+    """Walk the packed tokens in order and cut them into (trajectory, turn) runs.
+
+    success: optional per-token outcome flags (nonzero = the trajectory
+    succeeded), checked to be constant over each trajectory's tokens."""
     traj_id = np.asarray(traj_id)
     turn_id = np.asarray(turn_id)
     loss_mask = np.asarray(loss_mask)
-    start, length, traj, turn, n_sup = [], [], [], [], []
+    flags = None if success is None else np.asarray(success)
+    start, length, traj, turn, n_sup, seg_flag = [], [], [], [], [], []
+    traj_flag = {}  # trajectory id -> flag of its first segment
     prev = None  # (traj, turn) of the previous token, None after padding
     for i in range(traj_id.shape[0]):
         b, t, m = int(traj_id[i]), int(turn_id[i]), int(loss_mask[i])
@@ -118,21 +146,29 @@ def segments(traj_id, turn_id, loss_mask, max_turns: int) -> Segments:
             continue
         if not 0 <= t < max_turns:
             return _failed(ERR_TURN_RANGE)
+        f = None if flags is None else int(flags[i] != 0)
         if prev != (b, t):
             if traj:
                 pb, pt = traj[-1], turn[-1]
                 if b < pb or (b == pb and t <= pt):
                     return _failed(ERR_UNSORTED)
+            if f is not None:
+                if traj_flag.setdefault(b, f) != f:
+                    return _failed(ERR_OUTCOME)
+                seg_flag.append(f)
             start.append(i)
             length.append(0)
             traj.append(b)
             turn.append(t)
             n_sup.append(0)
+        elif f is not None and f != seg_flag[-1]:
+            return _failed(ERR_OUTCOME)
         length[-1] += 1
         n_sup[-1] += 1 if m else 0
         prev = (b, t)
     a = lambda x: np.asarray(x, dtype=np.int64)
-    return Segments(OK, a(start), a(length), a(traj), a(turn), a(n_sup))
+    return Segments(OK, a(start), a(length), a(traj), a(turn), a(n_sup),
+                    None if flags is None else a(seg_flag))
 
 
 def _failed(code: int) -> Segments:
@@ -144,13 +180,31 @@ def _failed(code: int) -> Segments:
 # token weights (Sec. 5.2; App. D, Algorithm 1)
 
 
-def token_weights(seg: Segments, n_tokens: int, loss_mask, alpha: float) -> np.ndarray:
+def n_min_of(n_traj: int, floor: int, frac: float) -> int:
+    """n_min = max(floor, ceil(frac * n_traj)) (App. D, full-configuration
+    table: min_floor and min_frac of the internal blend)."""
+    return max(int(floor), math.ceil(float(frac) * float(n_traj)))
+
+
+def turn_survivors(seg: Segments, max_turns: int) -> np.ndarray:
+    """n_t: trajectories with at least one supervised token at turn t."""
+    n = np.zeros(max_turns, np.int64)
+    for s in range(seg.count):
+        if seg.n_sup[s] > 0:
+            n[int(seg.turn[s])] += 1
+    return n
+
+
+def token_weights(seg: Segments, n_tokens: int, loss_mask, alpha: float,
+                  floor: int = 0, frac: float = 0.0) -> np.ndarray:
     """w_i such that the batch loss is sum_i w_i * l_i.
 
     Per trajectory: q_traj_t = n_t / sum_j n_j, q_turn_t = 1 / T,
     q_blend_t = (1 - alpha) q_traj_t + alpha q_turn_t; the turn's weight is
     shared equally by its n_t supervised tokens, and trajectories are
-    averaged (seq-mean-token-mean).
+    averaged (seq-mean-token-mean).  With a support floor, the turn term
+    covers only the valid turns (survivors >= n_min): 1 / T_v on each, 0 on
+    the others, and the trajectory term when the trajectory has none.
     """
     loss_mask = np.asarray(loss_mask)
     w = np.zeros(n_tokens, np.float64)
@@ -161,14 +215,21 @@ def token_weights(seg: Segments, n_tokens: int, loss_mask, alpha: float) -> np.n
     if not live:
         return w
     n_live = len(live)
+    max_turn = int(seg.turn.max()) + 1
+    surv = turn_survivors(seg, max_turn)
+    n_min = n_min_of(n_live, floor, frac)
     for b in live:
         ss = [s for s in by_traj[b] if seg.n_sup[s] > 0]
         n_t = {s: int(seg.n_sup[s]) for s in ss}
         total = sum(n_t.values())          # N = sum_t n_t
-        n_turns = len(ss)                  # T, turns with supervision
+        valid = {s: surv[int(seg.turn[s])] >= n_min for s in ss}
+        n_valid = sum(valid.values())      # T_v; T when every turn is valid
         for s in ss:
             q_traj = n_t[s] / total
-            q_turn = 1.0 / n_turns
+            if n_valid:
+                q_turn = (1.0 / n_valid) if valid[s] else 0.0
+            else:
+                q_turn = q_traj
             q_blend = (1.0 - alpha) * q_traj + alpha * q_turn
             per_token = q_blend / n_t[s] / n_live
             lo, hi = int(seg.start[s]), int(seg.start[s] + seg.length[s])
@@ -214,10 +275,12 @@ def losses(w_blend: np.ndarray, w_traj: np.ndarray, w_turn: np.ndarray, kl: np.n
     return (float(np.sum(w_blend * kl)), float(np.sum(w_traj * kl)), float(np.sum(w_turn * kl)))
 
 
-def turn_stats(parts, max_turns: int) -> np.ndarray:
+def turn_stats(parts, max_turns: int, outcome=None) -> np.ndarray:
     """Per-turn-index statistics over one or more micro-batches.
 
-    parts: iterable of (seg, loss_mask, kl, w) per micro-batch.  Everything is
+    parts: iterable of (seg, loss_mask, kl, w) per micro-batch; outcome 0 or 1
+    keeps only the segments of failed or successful trajectories (their
+    flags in seg.success).  Everything is
     recomputed from the pooled per-token values (no merge formula):
       n_tokens[t]  supervised tokens at turn t
       n_traj[t]    trajectories with a supervised token at turn t (survivors)
@@ -231,6 +294,8 @@ def turn_stats(parts, max_turns: int) -> np.ndarray:
     for seg, loss_mask, kl, w in parts:
         loss_mask = np.asarray(loss_mask)
         for s in range(seg.count):
+            if outcome is not None and int(seg.success[s]) != int(outcome):
+                continue
             t = int(seg.turn[s])
             if seg.n_sup[s] > 0:
                 surv[t] += 1
@@ -276,27 +341,31 @@ class Result:
     loss: tuple              # (L_blend, L_traj, L_turn)
     stats: np.ndarray        # STAT_DTYPE [max_turns]
     grads: dict              # row -> unweighted dKL/dz_s float64 [V]; G = grad_scale * w[row] * g
+    outcome_stats: np.ndarray = None  # STAT_DTYPE [2, max_turns]: failed, successful
 
 
 def fwd_bwd(traj_id, turn_id, loss_mask, alpha: float, max_turns: int, row_source,
             dtype: int, grad_scale: float = 1.0, grad_rows=(), chunk_rows: int = 512,
-            n_threads: int = 0) -> Result:
+            n_threads: int = 0, support_floor: int = 0, support_frac: float = 0.0,
+            success=None) -> Result:
     """Reference for one call of the fused path.
 
     row_source(rows) -> (zs, zt): host arrays [len(rows), V] holding the
     listed rows (uint16 bf16 patterns or float32).  Only supervised rows are
     evaluated; rows listed in grad_rows also return their gradient.
+    support_floor, support_frac: the turn-support floor of the turn term;
+    success: per-token outcome flags (adds the per-outcome statistics).
     """
     traj_id = np.asarray(traj_id)
     loss_mask = np.asarray(loss_mask)
     n = int(traj_id.shape[0])
-    seg = segments(traj_id, turn_id, loss_mask, max_turns)
+    seg = segments(traj_id, turn_id, loss_mask, max_turns, success)
     if seg.status != OK:
         return Result(seg.status, seg, np.zeros(n), np.zeros(n), (np.nan,) * 3,
                       np.zeros(max_turns, STAT_DTYPE), {})
-    w = token_weights(seg, n, loss_mask, alpha)
-    w0 = token_weights(seg, n, loss_mask, 0.0)
-    w1 = token_weights(seg, n, loss_mask, 1.0)
+    w = token_weights(seg, n, loss_mask, alpha, support_floor, support_frac)
+    w0 = token_weights(seg, n, loss_mask, 0.0, support_floor, support_frac)
+    w1 = token_weights(seg, n, loss_mask, 1.0, support_floor, support_frac)
     kl = np.zeros(n, np.float64)
     sup = np.nonzero(loss_mask)[0]
     for k0 in range(0, sup.shape[0], chunk_rows):
@@ -312,4 +381,16 @@ def fwd_bwd(traj_id, turn_id, loss_mask, alpha: float, max_turns: int, row_sourc
         for k, r in enumerate(rows.tolist()):
             grads[r] = g[k]
     stats = turn_stats([(seg, loss_mask, kl, w)], max_turns)
-    return Result(OK, seg, w, kl, losses(w, w0, w1, kl), stats, grads)
+    return Result(OK, seg, w, kl, losses(w, w0, w1, kl), stats, grads,
+                  outcome_split(seg, loss_mask, kl, w, max_turns))
+
+
+def outcome_split(seg: Segments, loss_mask, kl, w, max_turns: int):
+    """Per-turn statistics of the failed (row 0) and successful (row 1)
+    trajectories (Sec. 4.2), or None without outcome flags."""
+    if seg.success is None:
+        return None
+    out = np.zeros((2, max_turns), STAT_DTYPE)
+    for f in (0, 1):
+        out[f] = turn_stats([(seg, loss_mask, kl, w)], max_turns, outcome=f)
+    return out
