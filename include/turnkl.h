@@ -67,6 +67,7 @@ typedef enum {
   TURNKL_ERR_HIP = -7,           /* a HIP runtime call failed */
   TURNKL_ERR_SYNC_TIMEOUT = -8,  /* device: cross-workgroup exchange did not complete */
   TURNKL_ERR_TOPK_ID = -9,       /* device: a top-K support id outside [0, vocab) */
+  TURNKL_ERR_OUTCOME = -10,      /* device: outcome flag not constant over a trajectory */
 } turnkl_status;
 
 /* Statistics of one turn index t over the supervised tokens at that turn. */
@@ -78,6 +79,46 @@ typedef struct {
   double kl_var;     /* kl_m2 / n_tokens (population variance); 0 if n_tokens == 0 */
   double loss_mass;  /* sum over those tokens of w_i * KL_i (turn t's share of L) */
 } turnkl_turn_stat;
+
+/*
+ * Optional variants of the weights and statistics, shared by turnkl_fwd_bwd
+ * and turnkl_fwd_bwd_topk.  A NULL options pointer, or a zeroed struct, means
+ * none of them.
+ *
+ * Turn-support floor (App. D, full-configuration table: the internal blend's
+ * min_floor = 8 and min_frac = 0.15 give n_min = max(min_floor,
+ * ceil(min_frac * n_traj)); Sec. 7.2 calls the turns that enough trajectories
+ * reach "valid turns").  The paper does not say how n_min enters the turn
+ * term; this library reads it as follows.  n_traj is B, the trajectories of
+ * the call with a supervised token, and frac * B is rounded once in double
+ * before the ceiling.  Turn t is valid when its survivor count n_t (the
+ * trajectories of the call with a supervised token at t) is >= n_min.  The
+ * turn term of trajectory b gives each of its T_vb valid supervised turns
+ * 1 / T_vb and its other turns 0; a trajectory with no valid supervised turn
+ * uses its trajectory term n_bt / N_b instead.  So
+ *   w_i = m_i / B * ((1 - alpha) / N_b + alpha * u_bt),
+ *   u_bt = [t valid] / (T_vb * n_bt) if T_vb > 0, else 1 / N_b,
+ * the weights still sum to 1, L_turn uses alpha = 1 of the same form and
+ * L_traj is unchanged.  support_floor = 0 with support_frac = 0 (or any
+ * n_min <= 1) gives the plain weights.
+ *
+ * Outcome split (Sec. 4.2: K_t^fail and K_t^succ, the per-turn KL means over
+ * failed and successful rollouts; G_t = K_t^fail - K_t^succ).  success holds
+ * one flag per token (nonzero = the trajectory succeeded; flags of padding
+ * tokens are ignored) and must be constant over each trajectory's tokens, or
+ * the device reports TURNKL_ERR_OUTCOME at the first token where it changes
+ * (after the other checks at that token).  outcome_stats_out receives the
+ * per-turn statistics of the failed trajectories' tokens in entries
+ * [0, max_turns) and of the successful ones' in [max_turns, 2 * max_turns),
+ * with the fields and the accumulate_stats rule of turn_stats_out; the two
+ * halves partition turn_stats_out's counts and loss mass.
+ */
+typedef struct {
+  int32_t support_floor;   /* >= 0; 0 with support_frac 0: no floor */
+  double support_frac;     /* in [0, 1] */
+  const uint8_t* success;  /* device [n_tokens] outcome flags, or NULL */
+  turnkl_turn_stat* outcome_stats_out;  /* device [2 * max_turns], or NULL */
+} turnkl_options;
 
 /*
  * Bytes of device workspace turnkl_fwd_bwd needs for this problem (host
@@ -126,13 +167,20 @@ size_t turnkl_workspace_bytes(int64_t n_tokens, int64_t vocab, int dtype, int32_
  *                                  they are); 0 overwrites.
  * token_kl_out                     [n_tokens] float per-token KL (0 for
  *                                  unsupervised tokens), or NULL.
+ * options                          host pointer to turnkl_options, or NULL.
+ *                                  success and outcome_stats_out go together
+ *                                  (success may be NULL when n_tokens == 0);
+ *                                  outcome_stats_out must not overlap
+ *                                  turn_stats_out (TURNKL_ERR_ALIAS).
  * workspace, workspace_bytes       scratch of at least turnkl_workspace_bytes().
  *
  * Weights: w_i = m_i / B * ((1 - alpha) / N_b + alpha / (T_b * n_bt)) for token
  * i of trajectory b at turn t, where n_bt is the supervised count of the
  * segment, N_b = sum_t n_bt, T_b = #{t : n_bt > 0} and B = #{b : N_b > 0}; the
- * weights sum to 1.  An empty batch or one without supervised tokens yields a
- * zero loss, a zero gradient and zero (or unchanged, when accumulating) stats.
+ * weights sum to 1.  A turn-support floor in `options` replaces the turn term
+ * as described at turnkl_options.  An empty batch or one without supervised
+ * tokens yields a zero loss, a zero gradient and zero (or unchanged, when
+ * accumulating) stats.
  *
  * Returns TURNKL_OK once everything is enqueued, or a negative host-detected
  * error with nothing enqueued.  Device-detected data errors are reported by
@@ -144,15 +192,17 @@ int turnkl_fwd_bwd(const void* student_logits, int64_t ld_student, const void* t
                    const int32_t* turn_id, const int32_t* traj_id, const uint8_t* loss_mask,
                    double alpha, float grad_scale, float* loss_out, void* grad_out,
                    int64_t ld_grad, turnkl_turn_stat* turn_stats_out, int32_t max_turns,
-                   int accumulate_stats, float* token_kl_out, void* workspace,
-                   size_t workspace_bytes, hipStream_t stream);
+                   int accumulate_stats, float* token_kl_out, const turnkl_options* options,
+                   void* workspace, size_t workspace_bytes, hipStream_t stream);
 
 /*
  * Waits for `stream`, then returns the device-side status of the last
  * turnkl_fwd_bwd call that used `workspace`: TURNKL_OK or a data error
- * (TURNKL_ERR_UNSORTED / _TURN_RANGE / _PAD_MASK; the earliest offending token
- * in token order decides, a range error before an ordering error on the same
- * token), or TURNKL_ERR_SYNC_TIMEOUT; TURNKL_ERR_HIP if the read-back fails.
+ * (TURNKL_ERR_UNSORTED / _TURN_RANGE / _PAD_MASK / _OUTCOME, or _TOPK_ID for
+ * the top-K call; the earliest offending token in token order decides; at one
+ * token a padding-mask error, then a range error, then an ordering error,
+ * then an outcome-flag error), or TURNKL_ERR_SYNC_TIMEOUT; TURNKL_ERR_HIP if
+ * the read-back fails.
  */
 int turnkl_get_status(const void* workspace, hipStream_t stream);
 
@@ -249,8 +299,8 @@ int turnkl_fwd_bwd_topk(const void* student_logits, int64_t ld_student, int dtyp
                         double alpha, float grad_scale, float* loss_out, void* grad_out,
                         int64_t ld_grad, float* grad_topk_out, int64_t ld_grad_topk,
                         turnkl_turn_stat* turn_stats_out, int32_t max_turns, int accumulate_stats,
-                        float* token_kl_out, void* workspace, size_t workspace_bytes,
-                        hipStream_t stream);
+                        float* token_kl_out, const turnkl_options* options, void* workspace,
+                        size_t workspace_bytes, hipStream_t stream);
 
 /* ------------------------------------------------------------------------
  * Adaptive rollout-depth controller (Sec. 5.1; App. D, Algorithm 1 and the

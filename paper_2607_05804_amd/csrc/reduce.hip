@@ -4,13 +4,15 @@
 //              segment's supervised KL (float64, fixed order), and the
 //              segment's shares of L_blend = sum_i w_i KL_i (App. D,
 //              Algorithm 1), L_traj (alpha = 0) and L_turn (alpha = 1).
-// finalize     one workgroup per turn index t: the segments of turn t merged
-//              in segment order (pairwise update of Chan, Golub & LeVeque for
-//              the mean and m2) -> pooled mean K_t (Sec. 4.3, Eq.
+// finalize     one workgroup per (group, turn index t): the segments of turn t
+//              merged in segment order (pairwise update of Chan, Golub &
+//              LeVeque for the mean and m2) -> pooled mean K_t (Sec. 4.3, Eq.
 //              observed-turn-kl), population variance, survivors n_t (Sec.
 //              5.1, App. D), loss mass (Sec. 4.4); optionally merged into the
-//              caller's running statistics.  One more workgroup sums the loss
-//              shares.  No floating-point atomics: results are reproducible.
+//              caller's running statistics.  Group 0 takes every trajectory;
+//              groups 1 and 2 the failed and the successful ones (Sec. 4.2:
+//              K_t^fail, K_t^succ).  One more workgroup sums the loss shares.
+//              No floating-point atomics: results are reproducible.
 
 #include "block_ops.h"
 #include "turnkl_internal.h"
@@ -27,6 +29,7 @@ __global__ __launch_bounds__(kMomThreads) void seg_moments(SegParams p, Ws ws, c
   if (ws.hdr->err_key != kNoError) return;
   const int n_seg = ws.hdr->n_seg;
   const double b = (double)ws.hdr->b_eff;
+  const int n_min = p.floor_on ? support_n_min(p, ws.hdr->b_eff) : 0;
   for (int s = blockIdx.x; s < n_seg; s += gridDim.x) {
     const int n = ws.seg_nsup[s];
     SegStat out{};
@@ -47,15 +50,16 @@ __global__ __launch_bounds__(kMomThreads) void seg_moments(SegParams p, Ws ws, c
       }
       m2 = block_sum<kMomThreads>(m2, s_red);
       const int h = ws.seg_head[s];
-      const double t_b = (double)ws.traj_T[h];
       const double n_b = (double)ws.traj_N[h];
-      const double w = ((1.0 - alpha) / n_b + alpha / (t_b * (double)n)) / b;
+      const TurnTerm u = turn_term(p, ws, s, h, n_min);
+      const double w = ((1.0 - alpha) / n_b + turn_part(alpha, u, (double)n, n_b)) / b;
       out.sum = sum;
       out.mean = mean;
       out.m2 = m2;
       out.lm = w * sum;
       out.ltraj = sum / (b * n_b);
-      out.lturn = sum / (b * t_b * (double)n);
+      if (u.t_v > 0.0) out.lturn = u.valid ? sum / (b * u.t_v * (double)n) : 0.0;
+      else out.lturn = sum / (b * n_b);
       out.n = n;
     }
     if (threadIdx.x == 0) {
@@ -89,13 +93,19 @@ __device__ inline Moments merge(const Moments& x, const Moments& y) {
   return r;
 }
 
+// Grid: 3 * max_turns + 1 workgroups (max_turns = 0 without statistics).
+// Workgroup j < 3 * max_turns handles group j / max_turns at turn
+// j % max_turns; the last one sums the losses.
 __global__ __launch_bounds__(kFinThreads) void finalize(Ws ws, int max_turns, float* loss_out,
-                                                       turnkl_turn_stat* stats, int accumulate) {
+                                                       turnkl_turn_stat* stats,
+                                                       turnkl_turn_stat* ostats,
+                                                       const unsigned char* success,
+                                                       int accumulate) {
   __shared__ Moments s_m[kFinThreads];
   __shared__ double s_l[3][kFinThreads];
   const bool bad = ws.hdr->err_key != kNoError;
   const int n_seg = ws.hdr->n_seg;
-  if ((int)blockIdx.x == max_turns) {  // the three losses
+  if ((int)blockIdx.x == 3 * max_turns) {  // the three losses
     if (bad) {
       if (threadIdx.x < 3) loss_out[threadIdx.x] = __builtin_nanf("");
       return;
@@ -121,11 +131,16 @@ __global__ __launch_bounds__(kFinThreads) void finalize(Ws ws, int max_turns, fl
     if (threadIdx.x < 3) loss_out[threadIdx.x] = (float)s_l[threadIdx.x][0];
     return;
   }
-  if (bad || stats == nullptr) return;
-  const int t = blockIdx.x;
+  const int group = (int)blockIdx.x / max_turns;
+  const int t = (int)blockIdx.x - group * max_turns;
+  turnkl_turn_stat* out = group == 0 ? stats : ostats;
+  if (bad || out == nullptr) return;
+  if (group > 0) out += (group - 1) * max_turns;
+  const bool want_success = group == 2;
   Moments acc{0.0, 0.0, 0.0, 0.0, 0};
   for (int s = threadIdx.x; s < n_seg; s += kFinThreads) {
     if (ws.seg_turn[s] != t) continue;
+    if (group > 0 && (success[ws.seg_start[s]] != 0) != want_success) continue;
     const SegStat& g = ws.seg_stat[s];
     if (g.n == 0) continue;
     acc = merge(acc, Moments{(double)g.n, g.mean, g.m2, g.lm, 1});
@@ -138,7 +153,7 @@ __global__ __launch_bounds__(kFinThreads) void finalize(Ws ws, int max_turns, fl
   }
   if (threadIdx.x != 0) return;
   Moments r = s_m[0];
-  turnkl_turn_stat& o = stats[t];
+  turnkl_turn_stat& o = out[t];
   if (accumulate && r.n == 0.0) return;  // nothing to merge at this turn
   if (accumulate) {
     const Moments old{(double)o.n_tokens, o.kl_mean, o.kl_m2, o.loss_mass, (long long)o.n_traj};
@@ -160,15 +175,16 @@ __global__ __launch_bounds__(kFinThreads) void finalize(Ws ws, int max_turns, fl
 }  // namespace
 
 hipError_t launch_reduce(const SegParams& p, const Ws& ws, const float* kl, double alpha,
-                         float* loss_out, turnkl_turn_stat* stats, int accumulate, hipStream_t s) {
+                         float* loss_out, turnkl_turn_stat* stats, turnkl_turn_stat* ostats,
+                         int accumulate, hipStream_t s) {
   if (p.n > 0) {
     long long g = p.n < 4096 ? p.n : 4096;
     seg_moments<<<dim3((unsigned)g), dim3(kMomThreads), 0, s>>>(p, ws, kl, alpha);
     if (hipError_t e = hipGetLastError(); e != hipSuccess) return e;
   }
-  const int turns = stats ? p.max_turns : 0;
-  finalize<<<dim3((unsigned)(turns + 1)), dim3(kFinThreads), 0, s>>>(ws, turns, loss_out, stats,
-                                                                    accumulate);
+  const int turns = (stats || ostats) ? p.max_turns : 0;
+  finalize<<<dim3((unsigned)(3 * turns + 1)), dim3(kFinThreads), 0, s>>>(
+      ws, turns, loss_out, stats, ostats, p.success, accumulate);
   return hipGetLastError();
 }
 

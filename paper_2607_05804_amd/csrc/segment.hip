@@ -15,9 +15,18 @@
 //   seg_write   per tile: segment index of every token, segment start / turn /
 //               trajectory / end, supervised counts (integer atomics).
 //   seg_link    per segment: ordering check against the previous segment,
-//               segment length, trajectory head segment, T_b, N_b and B.
+//               outcome-flag check against the trajectory's first segment,
+//               segment length, trajectory head segment, T_b, N_b and B, and
+//               the survivors n_t of the turn-support floor.
+//   seg_valid   (turn-support floor only) per segment: T_vb, the valid
+//               supervised turns of each trajectory (n_t >= n_min).
 //   token_weights per token: w_i and grad_scale * w_i, clears this call's
 //               per-token KL and the row kernel's exchange slots.
+//
+// With the floor (App. D's internal-blend n_min = max(min_floor,
+// ceil(min_frac * B)); the turn term covers only valid turns) the weight is
+//   w_i = m_i / B * ((1 - alpha) / N_b + alpha * u_bt),
+//   u_bt = [n_t >= n_min] / (T_vb * n_bt) if T_vb > 0, else 1 / N_b.
 
 #include "block_ops.h"
 #include "turnkl_internal.h"
@@ -42,6 +51,11 @@ __device__ inline TokenInfo inspect(const SegParams& p, long long i) {
   r.pad = false;
   if (t < 0 || t >= p.max_turns) r.err = err_key(i, kPrioTurnRange);
   r.start = (i == 0) || p.traj[i - 1] != b || p.turn[i - 1] != t;
+  // inside a segment the outcome flag must not change (segment starts are
+  // checked against the trajectory's first segment in seg_link)
+  if (p.success && !r.start && r.err == kNoError &&
+      ((p.success[i] != 0) != (p.success[i - 1] != 0)))
+    r.err = err_key(i, kPrioOutcome);
   return r;
 }
 
@@ -60,6 +74,7 @@ __global__ __launch_bounds__(kSegThreads) void seg_count(SegParams p, Ws ws) {
     ws.seg_nsup[i] = 0;
     ws.traj_T[i] = 0;
     ws.traj_N[i] = 0;
+    ws.traj_Tv[i] = 0;
   }
   cnt = wave_sum(cnt);
   err = wave_min_u64(err);
@@ -83,9 +98,10 @@ __global__ __launch_bounds__(kSegThreads) void seg_count(SegParams p, Ws ws) {
 
 constexpr int kScanThreads = 1024;
 
-__global__ __launch_bounds__(kScanThreads) void seg_offsets(Ws ws, long long nblk) {
+__global__ __launch_bounds__(kScanThreads) void seg_offsets(Ws ws, long long nblk, int n_surv) {
   __shared__ int s_scan[kScanThreads / kWave];
   __shared__ unsigned long long s_err[kScanThreads / kWave];
+  for (int t = threadIdx.x; t < n_surv; t += kScanThreads) ws.turn_surv[t] = 0;
   int carry = 0;
   unsigned long long err = kNoError;
   for (long long b0 = 0; b0 < nblk; b0 += kScanThreads) {
@@ -145,7 +161,7 @@ __global__ __launch_bounds__(kSegThreads) void seg_write(SegParams p, Ws ws) {
   }
 }
 
-__global__ __launch_bounds__(kSegThreads) void seg_link(Ws ws) {
+__global__ __launch_bounds__(kSegThreads) void seg_link(SegParams p, Ws ws) {
   const int n_seg = ws.hdr->n_seg;
   for (int s = blockIdx.x * kSegThreads + threadIdx.x; s < n_seg; s += gridDim.x * kSegThreads) {
     const int b = ws.seg_traj[s];
@@ -165,11 +181,26 @@ __global__ __launch_bounds__(kSegThreads) void seg_link(Ws ws) {
     }
     const int head = lo;
     ws.seg_head[s] = head;
+    // On a sorted prefix `head` is the trajectory's first segment; otherwise
+    // an ordering error at or before this segment's start outranks this one.
+    if (p.success && head != s && (p.success[start] != 0) != (p.success[ws.seg_start[head]] != 0))
+      atomicMin(&ws.hdr->err_key, err_key(start, kPrioOutcome));
     const int n = ws.seg_nsup[s];
     if (n > 0) {
       atomicAdd(&ws.traj_T[head], 1);
       if (atomicAdd(&ws.traj_N[head], n) == 0) atomicAdd(&ws.hdr->b_eff, 1);
+      if (p.floor_on && t >= 0 && t < p.max_turns) atomicAdd(&ws.turn_surv[t], 1);
     }
+  }
+}
+
+__global__ __launch_bounds__(kSegThreads) void seg_valid(SegParams p, Ws ws) {
+  if (ws.hdr->err_key != kNoError) return;
+  const int n_seg = ws.hdr->n_seg;
+  const int n_min = support_n_min(p, ws.hdr->b_eff);
+  for (int s = blockIdx.x * kSegThreads + threadIdx.x; s < n_seg; s += gridDim.x * kSegThreads) {
+    if (ws.seg_nsup[s] > 0 && ws.turn_surv[ws.seg_turn[s]] >= n_min)
+      atomicAdd(&ws.traj_Tv[ws.seg_head[s]], 1);
   }
 }
 
@@ -178,6 +209,7 @@ __global__ __launch_bounds__(kSegThreads) void token_weights(SegParams p, Ws ws,
                                                              float* kl) {
   if (ws.hdr->err_key != kNoError) return;
   const double inv_b = ws.hdr->b_eff > 0 ? 1.0 / (double)ws.hdr->b_eff : 0.0;
+  const int n_min = p.floor_on ? support_n_min(p, ws.hdr->b_eff) : 0;
   for (long long i = (long long)blockIdx.x * kSegThreads + threadIdx.x; i < p.n;
        i += (long long)gridDim.x * kSegThreads) {
     kl[i] = 0.0f;
@@ -189,9 +221,9 @@ __global__ __launch_bounds__(kSegThreads) void token_weights(SegParams p, Ws ws,
     const int s = ws.tok_seg[i];
     const int h = ws.seg_head[s];
     const double n_bt = (double)ws.seg_nsup[s];
-    const double t_b = (double)ws.traj_T[h];
     const double n_b = (double)ws.traj_N[h];
-    const double w = inv_b * ((1.0 - alpha) / n_b + alpha / (t_b * n_bt));
+    const TurnTerm u = turn_term(p, ws, s, h, n_min);
+    const double w = inv_b * ((1.0 - alpha) / n_b + turn_part(alpha, u, n_bt, n_b));
     ws.w[i] = (float)w;
     ws.wsc[i] = (float)(w * (double)grad_scale);
     if (slot_words) {
@@ -215,12 +247,15 @@ hipError_t launch_segments(const SegParams& p, const Ws& ws, long long nblk, hip
     seg_count<<<dim3((unsigned)nblk), dim3(kSegThreads), 0, s>>>(p, ws);
     if (hipError_t e = hipGetLastError(); e != hipSuccess) return e;
   }
-  seg_offsets<<<1, kScanThreads, 0, s>>>(ws, nblk);
+  seg_offsets<<<1, kScanThreads, 0, s>>>(ws, nblk, p.floor_on ? p.max_turns : 0);
   if (hipError_t e = hipGetLastError(); e != hipSuccess) return e;
   if (nblk == 0) return hipSuccess;
   seg_write<<<dim3((unsigned)nblk), dim3(kSegThreads), 0, s>>>(p, ws);
   if (hipError_t e = hipGetLastError(); e != hipSuccess) return e;
-  seg_link<<<grid_for(p.n, kSegThreads, 1024), kSegThreads, 0, s>>>(ws);
+  seg_link<<<grid_for(p.n, kSegThreads, 1024), kSegThreads, 0, s>>>(p, ws);
+  if (hipError_t e = hipGetLastError(); e != hipSuccess) return e;
+  if (!p.floor_on) return hipSuccess;
+  seg_valid<<<grid_for(p.n, kSegThreads, 1024), kSegThreads, 0, s>>>(p, ws);
   return hipGetLastError();
 }
 

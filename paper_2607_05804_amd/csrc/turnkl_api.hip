@@ -76,6 +76,32 @@ size_t matrix_bytes(long long rows, long long ld, long long vocab, size_t es) {
   return rows > 0 ? (size_t)((rows - 1) * ld + vocab) * es : 0;
 }
 
+// Validates the options shared by both fused entry points and fills the
+// segment parameters they imply.  Returns TURNKL_OK or the error code.
+int apply_options(const turnkl_options* o, long long n_tokens, int max_turns,
+                  const turnkl_turn_stat* turn_stats_out, SegParams* sp,
+                  turnkl_turn_stat** outcome_stats_out) {
+  *outcome_stats_out = nullptr;
+  if (!o) return TURNKL_OK;
+  if (o->support_floor < 0) return TURNKL_ERR_INVALID_ARG;
+  if (!(o->support_frac >= 0.0 && o->support_frac <= 1.0)) return TURNKL_ERR_INVALID_ARG;
+  if (o->success && !o->outcome_stats_out) return TURNKL_ERR_INVALID_ARG;
+  if (o->outcome_stats_out && !o->success && n_tokens > 0) return TURNKL_ERR_INVALID_ARG;
+  if (o->outcome_stats_out && turn_stats_out &&
+      overlaps(o->outcome_stats_out, 2 * (size_t)max_turns * sizeof(turnkl_turn_stat),
+               turn_stats_out, (size_t)max_turns * sizeof(turnkl_turn_stat)))
+    return TURNKL_ERR_ALIAS;
+  sp->floor_on = o->support_floor > 0 || o->support_frac > 0.0;
+  sp->floor = o->support_floor;
+  sp->frac = o->support_frac;
+  sp->success = o->outcome_stats_out ? o->success : nullptr;
+  *outcome_stats_out = o->outcome_stats_out;
+  return TURNKL_OK;
+}
+
+// max_turns bounds: the statistics kernel runs 3 * max_turns + 1 workgroups.
+constexpr int kMaxTurns = (0x7FFFFFFF - 1) / 3;
+
 }  // namespace
 }  // namespace turnkl
 
@@ -84,9 +110,9 @@ using namespace turnkl;
 extern "C" {
 
 size_t turnkl_workspace_bytes(int64_t n_tokens, int64_t vocab, int dtype, int32_t max_turns) {
-  if (n_tokens < 0 || vocab < 1 || max_turns < 1) return 0;
+  if (n_tokens < 0 || vocab < 1 || max_turns < 1 || max_turns > kMaxTurns) return 0;
   if (dtype != TURNKL_BF16 && dtype != TURNKL_F32) return 0;
-  return make_layout(n_tokens, workspace_chunks(vocab, dtype)).total;
+  return make_layout(n_tokens, workspace_chunks(vocab, dtype), 0, max_turns).total;
 }
 
 int turnkl_fwd_bwd(const void* student_logits, int64_t ld_student, const void* teacher_logits,
@@ -94,11 +120,12 @@ int turnkl_fwd_bwd(const void* student_logits, int64_t ld_student, const void* t
                    const int32_t* turn_id, const int32_t* traj_id, const uint8_t* loss_mask,
                    double alpha, float grad_scale, float* loss_out, void* grad_out,
                    int64_t ld_grad, turnkl_turn_stat* turn_stats_out, int32_t max_turns,
-                   int accumulate_stats, float* token_kl_out, void* workspace,
-                   size_t workspace_bytes, hipStream_t stream) {
+                   int accumulate_stats, float* token_kl_out, const turnkl_options* options,
+                   void* workspace, size_t workspace_bytes, hipStream_t stream) {
   // ---- arguments
   if (dtype != TURNKL_BF16 && dtype != TURNKL_F32) return TURNKL_ERR_INVALID_ARG;
-  if (n_tokens < 0 || n_tokens > 0x7FFFFFFFll || vocab < 1 || max_turns < 1)
+  if (n_tokens < 0 || n_tokens > 0x7FFFFFFFll || vocab < 1 || max_turns < 1 ||
+      max_turns > kMaxTurns)
     return TURNKL_ERR_INVALID_ARG;
   if (!(alpha >= 0.0 && alpha <= 1.0)) return TURNKL_ERR_INVALID_ARG;  // rejects NaN
   if (!isfinite(grad_scale)) return TURNKL_ERR_INVALID_ARG;
@@ -139,13 +166,17 @@ int turnkl_fwd_bwd(const void* student_logits, int64_t ld_student, const void* t
   if ((unsigned long long)n_tokens * (unsigned long long)tiling.n_chunks > 0x7FFFFFFFull)
     return TURNKL_ERR_INVALID_ARG;
 
-  const Layout L = make_layout(n_tokens, workspace_chunks(vocab, dtype));
+  SegParams sp{traj_id, turn_id, loss_mask, nullptr, (long long)n_tokens, max_turns, 0, 0, 0.0};
+  turnkl_turn_stat* outcome_stats = nullptr;
+  if (int rc = apply_options(options, n_tokens, max_turns, turn_stats_out, &sp, &outcome_stats))
+    return rc;
+
+  const Layout L = make_layout(n_tokens, workspace_chunks(vocab, dtype), 0, max_turns);
   if (workspace_bytes < L.total) return TURNKL_ERR_WORKSPACE;
   const Ws ws = bind(workspace, L);
   float* kl = token_kl_out ? token_kl_out : ws.kl;
 
   // ---- launches
-  const SegParams sp{traj_id, turn_id, loss_mask, (long long)n_tokens, max_turns};
   if (launch_segments(sp, ws, L.nblk, stream) != hipSuccess) return TURNKL_ERR_HIP;
   if (launch_weights(sp, ws, alpha, grad_scale, tiling.n_chunks, kl, stream) != hipSuccess)
     return TURNKL_ERR_HIP;
@@ -171,15 +202,15 @@ int turnkl_fwd_bwd(const void* student_logits, int64_t ld_student, const void* t
   if (launch_rows(rp, tiling, stream) != hipSuccess) return TURNKL_ERR_HIP;
   if (prof && hipEventRecord(t_row_after, stream) != hipSuccess) return TURNKL_ERR_HIP;
 
-  if (launch_reduce(sp, ws, kl, alpha, loss_out, turn_stats_out, accumulate_stats, stream) !=
-      hipSuccess)
+  if (launch_reduce(sp, ws, kl, alpha, loss_out, turn_stats_out, outcome_stats, accumulate_stats,
+                    stream) != hipSuccess)
     return TURNKL_ERR_HIP;
   return TURNKL_OK;
 }
 
 size_t turnkl_topk_workspace_bytes(int64_t n_tokens, int32_t k, int32_t max_turns) {
-  if (n_tokens < 0 || k < 1 || k > kMaxTopK || max_turns < 1) return 0;
-  return make_layout(n_tokens, 0, k).total;
+  if (n_tokens < 0 || k < 1 || k > kMaxTopK || max_turns < 1 || max_turns > kMaxTurns) return 0;
+  return make_layout(n_tokens, 0, k, max_turns).total;
 }
 
 int turnkl_fwd_bwd_topk(const void* student_logits, int64_t ld_student, int dtype,
@@ -189,12 +220,13 @@ int turnkl_fwd_bwd_topk(const void* student_logits, int64_t ld_student, int dtyp
                         double alpha, float grad_scale, float* loss_out, void* grad_out,
                         int64_t ld_grad, float* grad_topk_out, int64_t ld_grad_topk,
                         turnkl_turn_stat* turn_stats_out, int32_t max_turns, int accumulate_stats,
-                        float* token_kl_out, void* workspace, size_t workspace_bytes,
-                        hipStream_t stream) {
+                        float* token_kl_out, const turnkl_options* options, void* workspace,
+                        size_t workspace_bytes, hipStream_t stream) {
   // ---- arguments
   if (dtype != TURNKL_BF16 && dtype != TURNKL_F32) return TURNKL_ERR_INVALID_ARG;
   const size_t es = dtype == TURNKL_BF16 ? 2 : 4;
-  if (n_tokens < 0 || n_tokens > 0x7FFFFFFFll || vocab < 1 || max_turns < 1)
+  if (n_tokens < 0 || n_tokens > 0x7FFFFFFFll || vocab < 1 || max_turns < 1 ||
+      max_turns > kMaxTurns)
     return TURNKL_ERR_INVALID_ARG;
   if ((unsigned long long)vocab * es > 0x7FFFFFFFull) return TURNKL_ERR_INVALID_ARG;
   if (k < 1 || k > kMaxTopK || k > vocab) return TURNKL_ERR_INVALID_ARG;
@@ -230,13 +262,16 @@ int turnkl_fwd_bwd_topk(const void* student_logits, int64_t ld_student, int dtyp
         return TURNKL_ERR_ALIAS;
     }
   }
-  const Layout L = make_layout(n_tokens, 0, k);
+  SegParams sp{traj_id, turn_id, loss_mask, nullptr, (long long)n_tokens, max_turns, 0, 0, 0.0};
+  turnkl_turn_stat* outcome_stats = nullptr;
+  if (int rc = apply_options(options, n_tokens, max_turns, turn_stats_out, &sp, &outcome_stats))
+    return rc;
+  const Layout L = make_layout(n_tokens, 0, k, max_turns);
   if (workspace_bytes < L.total) return TURNKL_ERR_WORKSPACE;
   const Ws ws = bind(workspace, L);
   float* kl = token_kl_out ? token_kl_out : ws.kl;
 
   // ---- launches
-  const SegParams sp{traj_id, turn_id, loss_mask, (long long)n_tokens, max_turns};
   if (launch_segments(sp, ws, L.nblk, stream) != hipSuccess) return TURNKL_ERR_HIP;
   if (launch_weights(sp, ws, alpha, grad_scale, 0, kl, stream) != hipSuccess) return TURNKL_ERR_HIP;
   TopkParams tp{};
@@ -263,8 +298,8 @@ int turnkl_fwd_bwd_topk(const void* student_logits, int64_t ld_student, int dtyp
   if (launch_topk_rows(tp, stream) != hipSuccess) return TURNKL_ERR_HIP;
   if (launch_topk_dense(tp, stream) != hipSuccess) return TURNKL_ERR_HIP;
   if (prof && hipEventRecord(t_row_after, stream) != hipSuccess) return TURNKL_ERR_HIP;
-  if (launch_reduce(sp, ws, kl, alpha, loss_out, turn_stats_out, accumulate_stats, stream) !=
-      hipSuccess)
+  if (launch_reduce(sp, ws, kl, alpha, loss_out, turn_stats_out, outcome_stats, accumulate_stats,
+                    stream) != hipSuccess)
     return TURNKL_ERR_HIP;
   return TURNKL_OK;
 }
@@ -323,6 +358,7 @@ const char* turnkl_status_string(int status) {
     case TURNKL_ERR_HIP: return "HIP runtime error";
     case TURNKL_ERR_SYNC_TIMEOUT: return "row exchange timed out";
     case TURNKL_ERR_TOPK_ID: return "top-K support id outside [0, vocab)";
+    case TURNKL_ERR_OUTCOME: return "outcome flag not constant over a trajectory";
     default: return "unknown status";
   }
 }

@@ -11,7 +11,8 @@ namespace turnkl {
 
 // ---------------------------------------------------------------------------
 // error keys: the earliest offending token wins; at one token a padding-mask
-// error, then a turn-range error, then an ordering error.
+// error, then a turn-range error, then an ordering error, then an outcome-flag
+// error.
 
 constexpr unsigned long long kNoError = ~0ull;
 enum : unsigned {
@@ -20,6 +21,7 @@ enum : unsigned {
   kPrioUnsorted = 2,
   kPrioTimeout = 3,
   kPrioTopkId = 4,  // top-K path: a support id outside [0, vocab)
+  kPrioOutcome = 5,  // outcome flag not constant over a trajectory
 };
 
 __host__ __device__ inline unsigned long long err_key(long long pos, unsigned prio) {
@@ -33,6 +35,7 @@ inline int status_from_key(unsigned long long key) {
     case kPrioTurnRange: return TURNKL_ERR_TURN_RANGE;
     case kPrioUnsorted: return TURNKL_ERR_UNSORTED;
     case kPrioTopkId: return TURNKL_ERR_TOPK_ID;
+    case kPrioOutcome: return TURNKL_ERR_OUTCOME;
     default: return TURNKL_ERR_SYNC_TIMEOUT;
   }
 }
@@ -69,7 +72,8 @@ constexpr int kSegTile = kSegThreads * kSegTokensPerThread;
 // that).
 struct Layout {
   size_t header, blk_cnt, blk_off, blk_err, tok_seg, seg_start, seg_len, seg_traj, seg_turn,
-      seg_nsup, seg_head, traj_T, traj_N, w, wsc, kl, seg_stat, slots, topk, total;
+      seg_nsup, seg_head, traj_T, traj_N, w, wsc, kl, seg_stat, slots, topk, traj_Tv, turn_surv,
+      total;
   long long nblk;
   int n_chunks;
 };
@@ -80,8 +84,9 @@ inline size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
 constexpr int kExchangeWords = 7;
 
 // n_chunks > 1: exchange slots of the full-vocabulary row kernel; topk_k > 0:
-// the top-K path's staging of the scaled gradient on each row's support.
-inline Layout make_layout(long long n_tokens, int n_chunks, int topk_k = 0) {
+// the top-K path's staging of the scaled gradient on each row's support;
+// max_turns: per-turn survivor counts of the turn-support floor.
+inline Layout make_layout(long long n_tokens, int n_chunks, int topk_k = 0, int max_turns = 0) {
   Layout L{};
   const size_t n = (size_t)n_tokens;
   L.nblk = (n_tokens + kSegTile - 1) / kSegTile;
@@ -107,6 +112,8 @@ inline Layout make_layout(long long n_tokens, int n_chunks, int topk_k = 0) {
   L.seg_stat = take(n * sizeof(SegStat));
   L.slots = take(n * (size_t)n_chunks * kExchangeWords * 8);
   L.topk = take(n * (size_t)topk_k * 4);
+  L.traj_Tv = take(n * 4);
+  L.turn_surv = take((size_t)max_turns * 4);
   L.total = o;
   return L;
 }
@@ -132,6 +139,8 @@ struct Ws {
   SegStat* seg_stat;
   unsigned long long* slots;
   float* topk;
+  int* traj_Tv;    // valid supervised turns of the trajectory (at its head segment)
+  int* turn_surv;  // survivors n_t per turn index
 };
 
 inline Ws bind(void* base, const Layout& L) {
@@ -156,6 +165,8 @@ inline Ws bind(void* base, const Layout& L) {
   w.seg_stat = reinterpret_cast<SegStat*>(b + L.seg_stat);
   w.slots = reinterpret_cast<unsigned long long*>(b + L.slots);
   w.topk = reinterpret_cast<float*>(b + L.topk);
+  w.traj_Tv = reinterpret_cast<int*>(b + L.traj_Tv);
+  w.turn_surv = reinterpret_cast<int*>(b + L.turn_surv);
   return w;
 }
 
@@ -188,9 +199,43 @@ struct SegParams {
   const int* traj;
   const int* turn;
   const unsigned char* mask;
+  const unsigned char* success;  // per-token outcome flags, or null
   long long n;
   int max_turns;
+  int floor_on;   // turn-support floor active (support_floor > 0 or support_frac > 0)
+  int floor;      // support_floor
+  double frac;    // support_frac
 };
+
+// n_min = max(floor, ceil(frac * B)), with frac * B rounded once in double.
+__host__ __device__ inline int support_n_min(const SegParams& p, int b_eff) {
+  const double c = ceil(p.frac * (double)b_eff);
+  return p.floor > (int)c ? p.floor : (int)c;
+}
+
+// The turn term of one supervised segment under the support floor: t_v is
+// T_vb (T_b without a floor) and `valid` says whether the segment's turn is
+// valid (always, without a floor).  u = [valid] / (t_v * n_bt) if t_v > 0,
+// else 1 / N_b; callers fold the constant factors in the order the plain
+// weights use, so that the floor-off results are unchanged bit for bit.
+struct TurnTerm {
+  double t_v;
+  bool valid;
+};
+
+// Segment s of the trajectory whose head segment is h; only called on a batch
+// without data errors (every turn id is in range).
+__device__ inline TurnTerm turn_term(const SegParams& p, const Ws& ws, int s, int h, int n_min) {
+  if (!p.floor_on) return TurnTerm{(double)ws.traj_T[h], true};
+  return TurnTerm{(double)ws.traj_Tv[h], ws.turn_surv[ws.seg_turn[s]] >= n_min};
+}
+
+// alpha * u for the segment (see TurnTerm) with n_bt supervised tokens and
+// N_b in its trajectory.
+__device__ inline double turn_part(double alpha, const TurnTerm& u, double n_bt, double n_b) {
+  if (u.t_v > 0.0) return u.valid ? alpha / (u.t_v * n_bt) : 0.0;
+  return alpha / n_b;
+}
 
 hipError_t launch_segments(const SegParams& p, const Ws& ws, long long nblk, hipStream_t s);
 hipError_t launch_weights(const SegParams& p, const Ws& ws, double alpha, float grad_scale,
@@ -249,7 +294,7 @@ hipError_t launch_topk_rows(const TopkParams& p, hipStream_t s);
 hipError_t launch_topk_dense(const TopkParams& p, hipStream_t s);
 
 hipError_t launch_reduce(const SegParams& p, const Ws& ws, const float* kl, double alpha,
-                         float* loss_out, turnkl_turn_stat* stats, int accumulate,
-                         hipStream_t s);
+                         float* loss_out, turnkl_turn_stat* stats, turnkl_turn_stat* ostats,
+                         int accumulate, hipStream_t s);
 
 }  // namespace turnkl

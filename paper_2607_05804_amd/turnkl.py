@@ -26,6 +26,7 @@ ERR_PAD_MASK = -6
 ERR_HIP = -7
 ERR_SYNC_TIMEOUT = -8
 ERR_TOPK_ID = -9
+ERR_OUTCOME = -10
 
 BF16 = 0
 F32 = 1
@@ -43,6 +44,12 @@ STAT_DTYPE = np.dtype([("n_tokens", "<i8"), ("n_traj", "<i8"), ("kl_mean", "<f8"
 STAT_FIELDS = 6  # int64, int64, 4 x float64 -> 48 bytes
 
 _lib = None
+
+
+class Options(ctypes.Structure):
+    """turnkl_options (include/turnkl.h)."""
+    _fields_ = [("support_floor", ctypes.c_int32), ("support_frac", ctypes.c_double),
+                ("success", ctypes.c_void_p), ("outcome_stats_out", ctypes.c_void_p)]
 
 
 class DepthConfig(ctypes.Structure):
@@ -80,8 +87,8 @@ def lib() -> ctypes.CDLL:
         l.turnkl_fwd_bwd.argtypes = [
             c.c_void_p, c.c_int64, c.c_void_p, c.c_int64, c.c_int, c.c_int64, c.c_int64,
             c.c_void_p, c.c_void_p, c.c_void_p, c.c_double, c.c_float, c.c_void_p, c.c_void_p,
-            c.c_int64, c.c_void_p, c.c_int32, c.c_int, c.c_void_p, c.c_void_p, c.c_size_t,
-            c.c_void_p]
+            c.c_int64, c.c_void_p, c.c_int32, c.c_int, c.c_void_p, c.POINTER(Options),
+            c.c_void_p, c.c_size_t, c.c_void_p]
         l.turnkl_get_status.restype = c.c_int
         l.turnkl_get_status.argtypes = [c.c_void_p, c.c_void_p]
         l.turnkl_get_segments.restype = c.c_int
@@ -102,7 +109,7 @@ def lib() -> ctypes.CDLL:
             c.c_void_p, c.c_int64, c.c_int, c.c_int64, c.c_int64, c.c_void_p, c.c_void_p,
             c.c_int64, c.c_int32, c.c_void_p, c.c_void_p, c.c_void_p, c.c_double, c.c_float,
             c.c_void_p, c.c_void_p, c.c_int64, c.c_void_p, c.c_int64, c.c_void_p, c.c_int32,
-            c.c_int, c.c_void_p, c.c_void_p, c.c_size_t, c.c_void_p]
+            c.c_int, c.c_void_p, c.POINTER(Options), c.c_void_p, c.c_size_t, c.c_void_p]
         l.turnkl_depth_default_config.restype = None
         l.turnkl_depth_default_config.argtypes = [c.POINTER(DepthConfig)]
         l.turnkl_depth_init.restype = c.c_int
@@ -141,6 +148,16 @@ def profile_row_kernel(before, after) -> None:
     b = ctypes.c_void_p(before.cuda_event) if before is not None else None
     a = ctypes.c_void_p(after.cuda_event) if after is not None else None
     lib().turnkl_profile_row_kernel(b, a)
+
+
+def _options(n: int, support_floor: int, support_frac: float, success, outcome_stats):
+    """turnkl_options for the keyword arguments, or None when all are off."""
+    if not support_floor and not support_frac and success is None and outcome_stats is None:
+        return None
+    if success is not None and (success.dtype != torch.uint8 or success.numel() != n):
+        raise ValueError("success must be uint8 with one entry per row")
+    return ctypes.byref(Options(int(support_floor), float(support_frac), _ptr(success),
+                                _ptr(outcome_stats)))
 
 
 def _dtype_code(t: torch.Tensor) -> int:
@@ -195,15 +212,20 @@ def fwd_bwd(student: torch.Tensor, teacher: torch.Tensor, turn_id: torch.Tensor,
             grad_scale: float = 1.0, grad: str | torch.Tensor | None = "new",
             max_turns: int = 64, turn_stats: torch.Tensor | None = None,
             accumulate_stats: bool = False, token_kl: bool | torch.Tensor = False,
-            workspace: Workspace | None = None, check: bool = True):
+            workspace: Workspace | None = None, check: bool = True, support_floor: int = 0,
+            support_frac: float = 0.0, success: torch.Tensor | None = None,
+            outcome_stats: torch.Tensor | None = None):
     """One fused forward + backward call on the current stream.
 
     grad: "new" allocates the gradient, "inplace" writes it over `student`,
     a tensor is used as the output, None computes the forward only.
     turn_stats: optional [max_turns * 6] float64-compatible device buffer in
     the turnkl_turn_stat layout (use new_turn_stats()); accumulate_stats
-    merges into it.  Returns (loss[3] tensor, grad or None, turn_stats or
-    None, token_kl or None, workspace).
+    merges into it.  support_floor / support_frac: the turn-support floor of
+    the turn term; success (uint8 per token) with outcome_stats (a
+    new_turn_stats(2 * max_turns) buffer: failed, then successful): the
+    per-outcome statistics (turnkl_options).  Returns (loss[3] tensor, grad or
+    None, turn_stats or None, token_kl or None, workspace).
     """
     dt = _dtype_code(student)
     if teacher.dtype != student.dtype:
@@ -237,7 +259,8 @@ def fwd_bwd(student: torch.Tensor, teacher: torch.Tensor, turn_id: torch.Tensor,
         _row_stride(teacher) if n else v, dt, n, v, _ptr(turn_id), _ptr(traj_id), _ptr(loss_mask),
         float(alpha), float(grad_scale), _ptr(loss), _ptr(grad_t),
         (_row_stride(grad_t) if n else v) if grad_t is not None else 0, _ptr(turn_stats),
-        int(max_turns), int(bool(accumulate_stats)), _ptr(kl_t), _ptr(workspace.tensor),
+        int(max_turns), int(bool(accumulate_stats)), _ptr(kl_t),
+        _options(n, support_floor, support_frac, success, outcome_stats), _ptr(workspace.tensor),
         workspace.nbytes, ctypes.c_void_p(stream))
     if rc != OK:
         raise TurnKLError(rc, "turnkl_fwd_bwd")
@@ -266,12 +289,15 @@ def fwd_bwd_topk(student: torch.Tensor, teacher_ids: torch.Tensor, teacher_vals:
                  grad: str | torch.Tensor | None = "new", grad_topk: bool | torch.Tensor = False,
                  max_turns: int = 64, turn_stats: torch.Tensor | None = None,
                  accumulate_stats: bool = False, token_kl: bool | torch.Tensor = False,
-                 workspace: TopkWorkspace | None = None, check: bool = True):
+                 workspace: TopkWorkspace | None = None, check: bool = True,
+                 support_floor: int = 0, support_frac: float = 0.0,
+                 success: torch.Tensor | None = None, outcome_stats: torch.Tensor | None = None):
     """The top-K variant (turnkl_fwd_bwd_topk) on the current stream.
 
     teacher_ids: int32 [N, K]; teacher_vals: float32 [N, K].  grad as in
     fwd_bwd (dense, zero off the support); grad_topk: True allocates, or a
-    float32 [N, K] tensor receives, the gradient on the support.  Returns
+    float32 [N, K] tensor receives, the gradient on the support; the options
+    as in fwd_bwd.  Returns
     (loss[3], grad or None, grad_topk or None, turn_stats or None,
     token_kl or None, workspace).
     """
@@ -318,7 +344,8 @@ def fwd_bwd_topk(student: torch.Tensor, teacher_ids: torch.Tensor, teacher_vals:
         float(grad_scale), _ptr(loss), _ptr(grad_t),
         (_row_stride(grad_t) if n else v) if grad_t is not None else 0, _ptr(gk),
         (int(gk.stride(0)) if n else k) if gk is not None else 0, _ptr(turn_stats),
-        int(max_turns), int(bool(accumulate_stats)), _ptr(kl_t), _ptr(workspace.tensor),
+        int(max_turns), int(bool(accumulate_stats)), _ptr(kl_t),
+        _options(n, support_floor, support_frac, success, outcome_stats), _ptr(workspace.tensor),
         workspace.nbytes, ctypes.c_void_p(stream))
     if rc != OK:
         raise TurnKLError(rc, "turnkl_fwd_bwd_topk")

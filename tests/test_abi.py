@@ -29,7 +29,7 @@ def test_every_declared_symbol_is_exported():
 
 def test_status_strings_and_alpha_schedule():
     assert T.status_string(T.OK) == "ok"
-    for code in range(-8, 0):
+    for code in range(-10, 0):
         assert T.status_string(code) != "unknown status"
     assert T.status_string(-99) == "unknown status"
     assert T.alpha_schedule(0, 100) == 0.0
@@ -46,6 +46,9 @@ def test_workspace_bytes():
     assert T.workspace_bytes(10, 0, T.BF16, 4) == 0
     assert T.workspace_bytes(10, 10, 7, 4) == 0
     assert T.workspace_bytes(10, 10, T.BF16, 0) == 0
+    assert T.workspace_bytes(10, 10, T.BF16, (2**31 - 2) // 3 + 1) == 0
+    # the per-turn survivor counts of the support floor grow with max_turns
+    assert T.workspace_bytes(10, 10, T.BF16, 4096) > T.workspace_bytes(10, 10, T.BF16, 4)
     a = T.workspace_bytes(1000, 151936, T.BF16, 50)
     b = T.workspace_bytes(2000, 151936, T.BF16, 50)
     assert 0 < a < b and a % 256 == 0
@@ -73,14 +76,22 @@ def _call(**kw):
     args = dict(zs=zs, ld_s=v, zt=zt, ld_t=v, dtype=T.BF16, n=n, v=v, turn=0x300000000,
                 traj=0x300100000, mask=0x300200000, alpha=0.5, scale=1.0, loss=0x300300000,
                 grad=0x400000000, ld_g=v, stats=0, max_turns=8, acc=0, kl=0,
-                ws=0x500000000, ws_bytes=ws_bytes)
+                ws=0x500000000, ws_bytes=ws_bytes, opts=None)
     args.update(kw)
     p = lambda x: ctypes.c_void_p(x) if x else None
     return T.lib().turnkl_fwd_bwd(
         p(args["zs"]), args["ld_s"], p(args["zt"]), args["ld_t"], args["dtype"], args["n"],
         args["v"], p(args["turn"]), p(args["traj"]), p(args["mask"]), args["alpha"],
         args["scale"], p(args["loss"]), p(args["grad"]), args["ld_g"], p(args["stats"]),
-        args["max_turns"], args["acc"], p(args["kl"]), p(args["ws"]), args["ws_bytes"], None)
+        args["max_turns"], args["acc"], p(args["kl"]), _opts(args["opts"]), p(args["ws"]),
+        args["ws_bytes"], None)
+
+
+def _opts(o):
+    """(support_floor, support_frac, success, outcome_stats_out) -> turnkl_options*."""
+    if o is None:
+        return None
+    return ctypes.byref(T.Options(o[0], o[1], o[2] or None, o[3] or None))
 
 
 @pytest.mark.parametrize("kw,code", [
@@ -112,6 +123,17 @@ def _call(**kw):
     # workspace too small or misaligned
     (dict(ws_bytes=1024), T.ERR_WORKSPACE),
     (dict(ws=0x500000010), T.ERR_WORKSPACE),
+    (dict(max_turns=(2**31 - 2) // 3 + 1), T.ERR_INVALID_ARG),
+    # options: floor and fraction ranges; success flags and outcome statistics
+    # go together; the outcome statistics must not overlap the turn statistics
+    (dict(opts=(-1, 0.0, 0, 0)), T.ERR_INVALID_ARG),
+    (dict(opts=(8, -0.1, 0, 0)), T.ERR_INVALID_ARG),
+    (dict(opts=(8, 1.5, 0, 0)), T.ERR_INVALID_ARG),
+    (dict(opts=(8, float("nan"), 0, 0)), T.ERR_INVALID_ARG),
+    (dict(opts=(0, 0.0, 0x700000000, 0)), T.ERR_INVALID_ARG),
+    (dict(opts=(0, 0.0, 0, 0x710000000)), T.ERR_INVALID_ARG),
+    (dict(stats=0x710000000, opts=(0, 0.0, 0x700000000, 0x710000000 + 48 * 7)), T.ERR_ALIAS),
+    (dict(stats=0x710000000 + 48 * 15, opts=(0, 0.0, 0x700000000, 0x710000000)), T.ERR_ALIAS),
 ])
 def test_host_rejects_bad_arguments_before_launch(kw, code):
     assert _call(**kw) == code
@@ -132,7 +154,7 @@ def _call_topk(**kw):
                 vals=0x210000000, ld_k=k, k=k, turn=0x300000000, traj=0x300100000,
                 mask=0x300200000, alpha=0.5, scale=1.0, loss=0x300300000, grad=0x400000000,
                 ld_g=v, gk=0x600000000, ld_gk=k, stats=0, max_turns=8, acc=0, kl=0,
-                ws=0x500000000, ws_bytes=ws_bytes)
+                ws=0x500000000, ws_bytes=ws_bytes, opts=None)
     args.update(kw)
     p = lambda x: ctypes.c_void_p(x) if x else None
     return T.lib().turnkl_fwd_bwd_topk(
@@ -140,7 +162,7 @@ def _call_topk(**kw):
         p(args["vals"]), args["ld_k"], args["k"], p(args["turn"]), p(args["traj"]), p(args["mask"]),
         args["alpha"], args["scale"], p(args["loss"]), p(args["grad"]), args["ld_g"], p(args["gk"]),
         args["ld_gk"], p(args["stats"]), args["max_turns"], args["acc"], p(args["kl"]),
-        p(args["ws"]), args["ws_bytes"], None)
+        _opts(args["opts"]), p(args["ws"]), args["ws_bytes"], None)
 
 
 def test_topk_workspace_bytes():
@@ -170,6 +192,8 @@ def test_topk_workspace_bytes():
     (dict(gk=0x100000000), T.ERR_ALIAS),
     (dict(gk=0x400000000 + 4096), T.ERR_ALIAS),
     (dict(ws_bytes=1024), T.ERR_WORKSPACE),
+    (dict(opts=(-3, 0.0, 0, 0)), T.ERR_INVALID_ARG),
+    (dict(opts=(0, 0.0, 0x700000000, 0)), T.ERR_INVALID_ARG),
 ])
 def test_topk_host_rejects_bad_arguments_before_launch(kw, code):
     assert _call_topk(**kw) == code
