@@ -163,6 +163,71 @@ def topk_timing(T, zs, zt, turn, traj, mask, w, steps: int, warmup: int, k: int 
     return out, host + (zs_at,)
 
 
+def options_timing(T, zs, zt, turn, traj, mask, w, grad, steps: int, warmup: int):
+    """The fused call with App. D's turn-support floor (8, 0.15) and the
+    per-outcome statistics (success flags: the even-numbered trajectories
+    stand in for the successful ones), timed against the plain call in the
+    same process, alternating.  Both variants add only work outside the row
+    kernel (one segment kernel, 2 * max_turns statistics workgroups), so the
+    comparison is of everything around the row kernel."""
+    import numpy as np
+    import torch
+    dev = zs.device
+    succ = torch.from_numpy((w.traj_id % 2 == 0).astype(np.uint8)).to(dev)
+    stats = T.new_turn_stats(w.max_turns, device=dev)
+    ostats = T.new_turn_stats(2 * w.max_turns, device=dev)
+    ws = T.Workspace(zs.shape[0], zs.shape[1], T.BF16, w.max_turns, device=dev)
+
+    def step(opt):
+        kw = dict(support_floor=8, support_frac=0.15, success=succ, outcome_stats=ostats) \
+            if opt else {}
+        return T.fwd_bwd(zs, zt, turn, traj, mask, w.alphas[0], grad=grad, max_turns=w.max_turns,
+                         turn_stats=stats, workspace=ws, check=False, **kw)
+
+    for _ in range(warmup):
+        step(False)
+        step(True)
+    torch.cuda.synchronize()
+    mk = lambda: torch.cuda.Event(enable_timing=True)
+    rec = {False: [], True: []}
+    for _ in range(steps):
+        for opt in (False, True):
+            a, ra, rb, b = mk(), mk(), mk(), mk()
+            a.record()
+            T.profile_row_kernel(ra, rb)
+            step(opt)
+            T.profile_row_kernel(None, None)
+            b.record()
+            rec[opt].append((a, ra, rb, b))
+    torch.cuda.synchronize()
+    if ws.status() != T.OK:
+        raise RuntimeError(T.status_string(ws.status()))
+
+    def summary(evs):
+        call = [a.elapsed_time(b) for a, _, _, b in evs]
+        row = [ra.elapsed_time(rb) for _, ra, rb, _ in evs]
+        return float(np.median(call)), float(np.median(call) - np.median(row))
+
+    plain_ms, plain_other = summary(rec[False])
+    opt_ms, opt_other = summary(rec[True])
+    st = T.read_turn_stats(stats)
+    n_b = int(np.unique(w.traj_id[(w.traj_id >= 0) & (w.loss_mask > 0)]).size)
+    n_min = max(8, int(np.ceil(0.15 * n_b)))
+    budget = T.budget_report(st, n_b, 8, 0.15)
+    gap = T.outcome_gap(ostats)
+    del ws
+    return {"support_floor": 8, "support_frac": 0.15, "n_min": n_min,
+            "valid_turns": int(np.sum(st["n_traj"] >= n_min)),
+            "supervised_turns": int(np.sum(st["n_traj"] > 0)),
+            "budget": {k: budget[k] for k in ("prefix", "third", "shallow_budget", "deep_budget",
+                                              "deep_support", "deep_shallow_kl")},
+            "outcome_gap_turns_0_to_4": [None if np.isnan(x) else float(x) for x in gap[:5]],
+            "call_ms_median": opt_ms, "plain_call_ms_median": plain_ms,
+            "outside_row_kernel_ms": opt_other, "plain_outside_row_kernel_ms": plain_other,
+            "note": "floor and outcome split on vs off, alternating in one process; the "
+                    "difference is the cost of the two options"}
+
+
 def oracle_topk_timing(w, host):
     """The top-K oracle on the whole batch (CPU baseline of the top-K path)."""
     from oracle import topk_oracle as K
@@ -305,6 +370,8 @@ def main() -> int:
     }
     out["depth_controller"] = depth_controller_timing(T, stats, w)
     stats_np = T.read_turn_stats(stats)
+    out["floor_and_outcome"] = options_timing(T, zs, zt, turn, traj, mask, w, grad, args.steps,
+                                              args.warmup)
     del grad
     torch.cuda.empty_cache()
     out["topk"], topk_host = topk_timing(T, zs, zt, turn, traj, mask, w, args.steps, args.warmup)

@@ -371,6 +371,53 @@ int turnkl_depth_update(const turnkl_depth_config* cfg, turnkl_depth_state* st,
                         const turnkl_turn_stat* stats, int32_t n_turns,
                         const int32_t* success_lengths, int64_t n_success);
 
+/* ------------------------------------------------------------------------
+ * Turn-level loss-allocation diagnostics (HOST functions over the per-turn
+ * statistics of one batch, as turnkl_fwd_bwd writes them, copied to the host).
+ *
+ *   s_t            Sec. 4.4: loss_mass[t] / sum_u loss_mass[u], the share of
+ *                  the batch's loss mass that turn t carries (s_t^traj when
+ *                  the statistics were taken at alpha = 0; the budget the
+ *                  blended objective spends otherwise, Sec. 7.2).  0 for every
+ *                  turn when the batch has no loss mass.
+ *   reliable prefix  the P leading turns t = 0, 1, ... whose survivor count
+ *                  n_t is at least max(n_min, 1), n_min = max(support_floor,
+ *                  ceil(support_frac * n_traj)) (App. D's floor formula; with
+ *                  (8, 0.10) and n_traj = n_0 it is the per-step part of the
+ *                  plotting rule of Sec. 4.1).
+ *   thirds         the first and the last ceil(P / 3) turns of the prefix.
+ *   Table 1 / 3    shallow and deep budget (sums of s_t over each third),
+ *                  deep support (mean over the deep third of n_t / n_0) and
+ *                  the deep/shallow raw-KL ratio (mean of K_t over the deep
+ *                  third / mean over the shallow third; NaN when P = 0 or the
+ *                  shallow mean is 0).
+ *   G_t            Sec. 4.2: K_t^fail - K_t^succ from the outcome statistics
+ *                  of turnkl_options; NaN where either outcome has no
+ *                  supervised token at turn t.
+ * All return TURNKL_OK, or TURNKL_ERR_INVALID_ARG for null pointers, n_turns
+ * < 1, n_traj < 0, support_floor < 0 or support_frac outside [0, 1].
+ * ------------------------------------------------------------------------ */
+typedef struct {
+  int64_t n_min;            /* support floor applied to the prefix */
+  int32_t prefix;           /* P */
+  int32_t third;            /* ceil(P / 3); 0 when P = 0 */
+  double shallow_budget;    /* sum of s_t over the shallow third */
+  double deep_budget;       /* sum of s_t over the deep third */
+  double deep_support;      /* mean of n_t / n_0 over the deep third */
+  double deep_shallow_kl;   /* mean K_t, deep third / shallow third */
+} turnkl_budget;
+
+/* share (host) [n_turns] receives s_t for stats (host) [n_turns]. */
+int turnkl_loss_share(const turnkl_turn_stat* stats, int32_t n_turns, double* share);
+
+/* The Table 1 / Table 3 figures of one batch into *out (host). */
+int turnkl_budget_report(const turnkl_turn_stat* stats, int32_t n_turns, int64_t n_traj,
+                         int32_t support_floor, double support_frac, turnkl_budget* out);
+
+/* gap (host) [n_turns] receives G_t from outcome_stats (host) [2 * n_turns]:
+ * failed trajectories first, then successful ones. */
+int turnkl_outcome_gap(const turnkl_turn_stat* outcome_stats, int32_t n_turns, double* gap);
+
 #ifdef __cplusplus
 }
 #endif

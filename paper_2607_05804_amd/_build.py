@@ -6,7 +6,8 @@ import sys
 HERE = os.path.dirname(os.path.abspath(__file__))
 ROOT = os.path.dirname(HERE)
 CSRC = os.path.join(HERE, "csrc")
-SOURCES = ["turnkl_api.hip", "segment.hip", "rowkl.hip", "reduce.hip", "topk.hip", "controller.cpp"]
+SOURCES = ["turnkl_api.hip", "segment.hip", "rowkl.hip", "reduce.hip", "topk.hip", "controller.cpp",
+           "diagnostics.cpp"]
 LIB = os.path.join(HERE, "libturnkl.so")
 
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")

@@ -37,7 +37,8 @@ EXPORTS = ("turnkl_workspace_bytes", "turnkl_fwd_bwd", "turnkl_get_status",
            "turnkl_profile_row_kernel", "turnkl_set_row_tiling",
            "turnkl_topk_workspace_bytes", "turnkl_fwd_bwd_topk",
            "turnkl_depth_default_config", "turnkl_depth_init", "turnkl_depth_plan",
-           "turnkl_depth_update")
+           "turnkl_depth_update", "turnkl_loss_share", "turnkl_budget_report",
+           "turnkl_outcome_gap")
 
 STAT_DTYPE = np.dtype([("n_tokens", "<i8"), ("n_traj", "<i8"), ("kl_mean", "<f8"),
                        ("kl_m2", "<f8"), ("kl_var", "<f8"), ("loss_mass", "<f8")])
@@ -65,6 +66,16 @@ class DepthState(ctypes.Structure):
     _fields_ = [("h_bar", ctypes.c_double), ("h_eff_bar", ctypes.c_double),
                 ("h_eff", ctypes.c_int32), ("h_cov", ctypes.c_int32),
                 ("h_ctrl", ctypes.c_int32), ("n_probes", ctypes.c_int32)]
+
+
+class Budget(ctypes.Structure):
+    """turnkl_budget (include/turnkl.h)."""
+    _fields_ = [("n_min", ctypes.c_int64), ("prefix", ctypes.c_int32), ("third", ctypes.c_int32),
+                ("shallow_budget", ctypes.c_double), ("deep_budget", ctypes.c_double),
+                ("deep_support", ctypes.c_double), ("deep_shallow_kl", ctypes.c_double)]
+
+    def as_dict(self) -> dict:
+        return {k: getattr(self, k) for k, _ in self._fields_}
 
 
 class TurnKLError(RuntimeError):
@@ -121,6 +132,13 @@ def lib() -> ctypes.CDLL:
         l.turnkl_depth_update.restype = c.c_int
         l.turnkl_depth_update.argtypes = [c.POINTER(DepthConfig), c.POINTER(DepthState), c.c_void_p,
                                           c.c_int32, c.c_void_p, c.c_int64]
+        l.turnkl_loss_share.restype = c.c_int
+        l.turnkl_loss_share.argtypes = [c.c_void_p, c.c_int32, c.c_void_p]
+        l.turnkl_budget_report.restype = c.c_int
+        l.turnkl_budget_report.argtypes = [c.c_void_p, c.c_int32, c.c_int64, c.c_int32, c.c_double,
+                                           c.POINTER(Budget)]
+        l.turnkl_outcome_gap.restype = c.c_int
+        l.turnkl_outcome_gap.argtypes = [c.c_void_p, c.c_int32, c.c_void_p]
         _lib = l
     return _lib
 
@@ -405,3 +423,40 @@ class DepthController:
                                          st.ctypes.data, st.shape[0],
                                          ln.ctypes.data if ln.size else None, ln.size),
                "turnkl_depth_update")
+
+
+def _host_stats(stats) -> np.ndarray:
+    if isinstance(stats, torch.Tensor):
+        stats = read_turn_stats(stats)
+    return np.ascontiguousarray(stats, dtype=STAT_DTYPE).reshape(-1)
+
+
+def loss_share(stats) -> np.ndarray:
+    """s_t of a batch's per-turn statistics (turnkl_loss_share; host code)."""
+    st = _host_stats(stats)
+    out = np.zeros(st.shape[0], np.float64)
+    _check(lib().turnkl_loss_share(st.ctypes.data, st.shape[0], out.ctypes.data),
+           "turnkl_loss_share")
+    return out
+
+
+def budget_report(stats, n_traj: int, support_floor: int = 8, support_frac: float = 0.15) -> dict:
+    """Deep/shallow budget, support and raw-KL ratio over the reliable turn
+    prefix (turnkl_budget_report; host code)."""
+    st = _host_stats(stats)
+    b = Budget()
+    _check(lib().turnkl_budget_report(st.ctypes.data, st.shape[0], int(n_traj), int(support_floor),
+                                      float(support_frac), ctypes.byref(b)),
+           "turnkl_budget_report")
+    return b.as_dict()
+
+
+def outcome_gap(outcome_stats) -> np.ndarray:
+    """G_t from the [2 * T] per-outcome statistics (turnkl_outcome_gap)."""
+    st = _host_stats(outcome_stats)
+    if st.shape[0] % 2:
+        raise ValueError("outcome statistics hold 2 * max_turns entries")
+    out = np.zeros(st.shape[0] // 2, np.float64)
+    _check(lib().turnkl_outcome_gap(st.ctypes.data, st.shape[0] // 2, out.ctypes.data),
+           "turnkl_outcome_gap")
+    return out

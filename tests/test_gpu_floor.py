@@ -9,6 +9,7 @@ import synth
 from gpu_support import (check_grad_rows, check_loss, check_segments, check_stats,
                          check_token_kl, device_row_source, ids_to_device, log, oracle_dtype,
                          sample_rows, to_device_logits)
+from oracle import diagnostics as D
 from oracle import topk_oracle as K
 from oracle import turnkl_oracle as O
 from paper_2607_05804_amd import turnkl as T
@@ -201,5 +202,20 @@ def test_long_horizon_full_size_with_the_paper_floor(gpu):
     _check_outcome(ostats, ref.outcome_stats, w.max_turns)
     worst = check_grad_rows(g, ref, 1.0, rows, w.loss_mask)
     log(f"  loss gpu={loss.tolist()} ref={ref.loss} grad err={worst:.1e}")
+    # the host diagnostics on the device statistics agree with the oracle's
+    # diagnostics on the oracle's statistics
+    n_b = int(np.unique(w.traj_id[(w.traj_id >= 0) & (w.loss_mask > 0)]).size)
+    got = T.budget_report(stats, n_b, 8, 0.15)
+    want = D.budget_report(ref.stats, n_b, 8, 0.15)
+    assert (got["n_min"], got["prefix"], got["third"]) == (want.n_min, want.prefix, want.third)
+    for k in ("shallow_budget", "deep_budget", "deep_support", "deep_shallow_kl"):
+        assert abs(got[k] - getattr(want, k)) <= 1e-4 * abs(getattr(want, k)) + 1e-7, k
+    np.testing.assert_allclose(T.loss_share(stats), D.loss_share(ref.stats), rtol=1e-4, atol=1e-8)
+    gap = T.outcome_gap(ostats)
+    want_gap = D.outcome_gap(ref.outcome_stats)
+    np.testing.assert_array_equal(np.isnan(gap), np.isnan(want_gap))
+    ok = ~np.isnan(want_gap)
+    np.testing.assert_allclose(gap[ok], want_gap[ok], rtol=1e-3, atol=1e-5)
+    log(f"  budget {got}")
     del zs, zt, g
     torch.cuda.empty_cache()
