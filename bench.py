@@ -30,10 +30,15 @@ COUNTER_FILE = os.path.join(ROOT, "profiles", "rowkl_long_horizon_counters.md")
 
 
 def row_kernel_digest() -> str:
+    """Digest of the row kernel's sources with comments and blank space
+    removed, so that it changes with the code and not with its comments."""
     h = hashlib.sha256()
     for p in ROW_KERNEL_SOURCES:
-        with open(os.path.join(ROOT, p), "rb") as f:
-            h.update(f.read())
+        with open(os.path.join(ROOT, p)) as f:
+            src = f.read()
+        src = re.sub(r"/\*.*?\*/", " ", src, flags=re.S)
+        src = re.sub(r"//[^\n]*", " ", src)
+        h.update(" ".join(src.split()).encode())
     return h.hexdigest()[:16]
 
 
@@ -189,16 +194,20 @@ def options_timing(T, zs, zt, turn, traj, mask, w, grad, steps: int, warmup: int
         step(True)
     torch.cuda.synchronize()
     mk = lambda: torch.cuda.Event(enable_timing=True)
-    rec = {False: [], True: []}
-    for _ in range(steps):
+    rec = {opt: [tuple(mk() for _ in range(4)) for _ in range(steps)] for opt in (False, True)}
+    for evs in rec.values():  # materialise the events before they are handed to the library
+        for e in evs:
+            for x in e:
+                x.record()
+    torch.cuda.synchronize()
+    for k in range(steps):
         for opt in (False, True):
-            a, ra, rb, b = mk(), mk(), mk(), mk()
+            a, ra, rb, b = rec[opt][k]
             a.record()
             T.profile_row_kernel(ra, rb)
             step(opt)
             T.profile_row_kernel(None, None)
             b.record()
-            rec[opt].append((a, ra, rb, b))
     torch.cuda.synchronize()
     if ws.status() != T.OK:
         raise RuntimeError(T.status_string(ws.status()))

@@ -15,10 +15,10 @@
 // into n_chunks balanced chunks (pack counts differ by at most one); each of
 // a workgroup's 256 threads holds up to vpt packs.  One workgroup owns one
 // (row, chunk) task: it loads its chunk of both rows into registers, reduces
-// the five partials, publishes them as tagged 64-bit words, reads its row
-// mates' words, merges all chunks in chunk order (so every workgroup of the
-// row computes bit-identical row scalars), and writes its chunk of the
-// gradient straight from registers.  Every logit is read from HBM exactly
+// the chunk's partials, publishes them as seven tagged 64-bit words (see the
+// row merge below), reads its row mates' words, merges all chunks in chunk
+// order (so every workgroup of the row computes bit-identical row scalars),
+// and writes its chunk of the gradient straight from registers.  Every logit is read from HBM exactly
 // once and every gradient element written once: 3 V s bytes per supervised
 // row, V s per unsupervised row (zeros only).
 //
