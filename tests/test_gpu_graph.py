@@ -13,8 +13,8 @@ from paper_2607_05804_amd import turnkl as T
 pytestmark = pytest.mark.gpu
 
 
-@pytest.mark.parametrize("vpt", [0, 4])
-def test_graph_replays_equal_eager(vpt, gpu):
+@pytest.mark.parametrize("vpt,opts", [(0, False), (4, False), (0, True)])
+def test_graph_replays_equal_eager(vpt, opts, gpu):
     w = synth.make("agent")
     zs_h, zt_h = w.host_logits(0, w.n_tokens)
     zs, zt = to_device_logits(zs_h), to_device_logits(zt_h)
@@ -26,24 +26,33 @@ def test_graph_replays_equal_eager(vpt, gpu):
         grad = torch.empty_like(zs)
         kl = torch.empty(n, dtype=torch.float32, device=gpu)
         stats = T.new_turn_stats(w.max_turns)
+        kw = {}
+        if opts:  # turn-support floor and outcome split
+            kw = dict(support_floor=8, support_frac=0.15,
+                      success=torch.from_numpy((w.traj_id % 2).astype(np.uint8)).to(gpu),
+                      outcome_stats=T.new_turn_stats(2 * w.max_turns))
         s = torch.cuda.Stream()
         s.wait_stream(torch.cuda.current_stream())
         with torch.cuda.stream(s):
             # eager reference on the side stream
             loss, _, _, _, _ = T.fwd_bwd(zs, zt, turn, traj, mask, 0.3, grad=grad,
                                          max_turns=w.max_turns, turn_stats=stats, token_kl=kl,
-                                         workspace=ws, check=False)
+                                         workspace=ws, check=False, **kw)
             s.synchronize()
-            ref = (loss.clone(), grad.clone(), kl.clone(), stats.clone())
+            ref = (loss.clone(), grad.clone(), kl.clone(), stats.clone(),
+                   kw["outcome_stats"].clone() if opts else None)
             g = torch.cuda.CUDAGraph()
             with torch.cuda.graph(g, stream=s):
                 loss_g, _, _, _, _ = T.fwd_bwd(zs, zt, turn, traj, mask, 0.3, grad=grad,
                                                max_turns=w.max_turns, turn_stats=stats,
-                                               token_kl=kl, workspace=ws, check=False)
+                                               token_kl=kl, workspace=ws, check=False, **kw)
         torch.cuda.current_stream().wait_stream(s)
         for r in range(4):
             grad.fill_(7)  # eager work between replays
             kl.zero_()
+            stats.fill_(5)
+            if opts:
+                kw["outcome_stats"].fill_(3)
             g.replay()
             torch.cuda.synchronize()
             assert ws.status() == T.OK
@@ -51,6 +60,8 @@ def test_graph_replays_equal_eager(vpt, gpu):
             assert torch.equal(grad.view(torch.int16), ref[1].view(torch.int16)), r
             assert torch.equal(kl, ref[2]), r
             assert torch.equal(stats, ref[3]), r
-        log(f"graph replays ok (vpt={vpt}): loss={loss_g.tolist()}")
+            if opts:
+                assert torch.equal(kw["outcome_stats"], ref[4]), r
+        log(f"graph replays ok (vpt={vpt}, options={opts}): loss={loss_g.tolist()}")
     finally:
         T.set_row_tiling(0)
