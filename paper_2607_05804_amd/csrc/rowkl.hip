@@ -290,9 +290,9 @@ __global__ __launch_bounds__(kRowThreads) void rowkl_kernel(RowParams p) {
   const int lane = tid & (kWave - 1);
   const int wid = tid / kWave;
   const unsigned n_tasks = (unsigned)p.n_rows * (unsigned)p.n_chunks;
-  // balanced chunks: chunk c is packs [n_packs c / n_chunks, n_packs (c + 1) / n_chunks)
+  // chunk c is packs [chunk_start(c), chunk_start(c + 1)) of the row
   for (int k = tid; k <= p.n_chunks; k += kRowThreads)
-    s_lo[k] = (int)((long long)p.n_packs * k / p.n_chunks);
+    s_lo[k] = (int)chunk_start(p.n_packs, p.n_chunks, p.align, k);
   // data of this wave's most recent 16-byte store, kept live until the next
   // task's loads are issued (see keep_alive)
   typename P::Data carry = P::zero();

@@ -28,10 +28,12 @@ long long ceil_div(long long a, long long b) { return (a + b - 1) / b; }
 
 int thread_tiling_override() { return t_vpt_override; }
 
-// Balanced chunks: k = ceil(P / (256 * vmax)) chunks of P / k packs (P packs
-// per row), and vpt = ceil(ceil(P / k) / 256) packs per thread.  Then every
-// chunk holds at least 256 * (vpt - 1) packs, which the row kernel relies on
-// (only a thread's last pack can fall outside its chunk).
+// k = ceil(P / (256 * vmax)) chunks of a row of P packs, with boundaries
+// from chunk_start: 1 KiB-aligned when that keeps vpt = ceil(widest / 256)
+// within vmax and every chunk at least 256 * (vpt - 1) packs long (the row
+// kernel relies on that: only a thread's last pack can fall outside its
+// chunk), else 128-byte-aligned, else balanced (chunks of P / k packs, for
+// which both conditions hold by construction).
 RowTiling vector_tiling(long long vocab, int dtype, int vmax) {
   RowTiling t{};
   t.vector = true;
@@ -39,9 +41,29 @@ RowTiling vector_tiling(long long vocab, int dtype, int vmax) {
   if (vmax == 0) vmax = kDefaultVmax;
   const long long packs = ceil_div(vocab, t.epv);
   t.n_chunks = (int)ceil_div(packs, (long long)kRowThreads * vmax);
-  const long long widest = ceil_div(packs, t.n_chunks);
-  t.vpt = (int)ceil_div(widest, kRowThreads);
-  t.chunk = widest * t.epv;
+  // balanced chunks: ceil(P / k) and floor(P / k) packs
+  t.align = 1;
+  t.min_chunk = packs / t.n_chunks;
+  t.vpt = (int)ceil_div(ceil_div(packs, t.n_chunks), kRowThreads);
+  t.chunk = ceil_div(packs, t.n_chunks) * t.epv;
+  if (t.n_chunks < 2 || t.n_chunks > kMaxChunks) return t;
+  for (int align : {64, 8}) {
+    long long widest = 0, narrowest = packs;
+    for (int c = 0; c < t.n_chunks; ++c) {
+      const long long w = chunk_start(packs, t.n_chunks, align, c + 1) -
+                          chunk_start(packs, t.n_chunks, align, c);
+      widest = w > widest ? w : widest;
+      narrowest = w < narrowest ? w : narrowest;
+    }
+    const int vpt = (int)ceil_div(widest, kRowThreads);
+    if (vpt <= vmax && narrowest >= 1 && narrowest >= (long long)kRowThreads * (vpt - 1)) {
+      t.align = align;
+      t.vpt = vpt;
+      t.chunk = widest * t.epv;
+      t.min_chunk = narrowest;
+      break;
+    }
+  }
   return t;
 }
 
@@ -52,6 +74,8 @@ RowTiling scalar_tiling(long long vocab) {
   t.vpt = kScalarVpt;
   t.n_chunks = (int)ceil_div(vocab, (long long)kRowThreads * kScalarVpt);
   t.chunk = ceil_div(vocab, t.n_chunks);
+  t.min_chunk = vocab / t.n_chunks;
+  t.align = 1;
   return t;
 }
 
@@ -156,7 +180,7 @@ int turnkl_fwd_bwd(const void* student_logits, int64_t ld_student, const void* t
     ok = ok && ((uintptr_t)student_logits & 15u) == 0 && ((uintptr_t)teacher_logits & 15u) == 0;
     if (grad_out) ok = ok && ld_grad % epv == 0 && ((uintptr_t)grad_out & 15u) == 0;
     const long long packs = vocab / epv;
-    ok = ok && packs / tiling.n_chunks >= (long long)kRowThreads * (tiling.vpt - 1);
+    ok = ok && tiling.min_chunk >= (long long)kRowThreads * (tiling.vpt - 1);
     if (!ok) tiling = scalar_tiling(vocab);
   }
   if (tiling.n_chunks > kMaxChunks) return TURNKL_ERR_INVALID_ARG;
@@ -196,6 +220,7 @@ int turnkl_fwd_bwd(const void* student_logits, int64_t ld_student, const void* t
   rp.n_rows = (int)n_tokens;
   rp.n_packs = (int)(vocab / tiling.epv);
   rp.n_chunks = tiling.n_chunks;
+  rp.align = tiling.align;
   rp.bf16 = dtype == TURNKL_BF16;
   const bool prof = t_row_before && t_row_after;
   if (prof && hipEventRecord(t_row_before, stream) != hipSuccess) return TURNKL_ERR_HIP;

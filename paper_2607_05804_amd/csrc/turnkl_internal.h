@@ -183,9 +183,25 @@ struct RowTiling {
   bool vector;  // 16-byte vector loads (aligned rows, vocab a multiple of the vector)
   int vpt;      // vectors (or scalar elements) per thread per chunk
   int epv;      // elements per vector (8 bf16, 4 fp32, 1 on the scalar path)
-  long long chunk;  // elements of a row handled by one workgroup
+  long long chunk;      // elements of the widest chunk
+  long long min_chunk;  // packs of the narrowest chunk
   int n_chunks;
+  int align;    // chunk boundaries are multiples of this many packs (see chunk_start)
 };
+
+// First pack of chunk c (0 <= c <= n_chunks) of a row of n_packs packs: the
+// balanced boundary n_packs c / n_chunks rounded up to a multiple of `align`
+// packs.  With align = 64 every interior boundary sits on a 1 KiB multiple
+// from the row start, so each wave's 1 KiB load or store covers whole cache
+// lines when rows start on a line; boundaries between lines made two waves
+// share a line and measured about 4% slower.  align = 1 gives balanced chunks.
+__host__ __device__ inline long long chunk_start(long long n_packs, int n_chunks, int align, int c) {
+  if (c <= 0) return 0;
+  if (c >= n_chunks) return n_packs;
+  const long long b = n_packs * c / n_chunks;
+  const long long r = (b + align - 1) / align * align;
+  return r < n_packs ? r : n_packs;
+}
 
 // Tiling of the vector path for a given vectors-per-thread (0 = automatic).
 RowTiling vector_tiling(long long vocab, int dtype, int vpt);
@@ -258,6 +274,7 @@ struct RowParams {
   int n_rows;
   int n_packs;   // vocab / elements per pack
   int n_chunks;  // <= kMaxChunks
+  int align;     // chunk boundary alignment in packs (chunk_start)
   int bf16;
 };
 

@@ -101,6 +101,10 @@ def check_all(out, ref, mask, grad_scale, rows):
     (1024, "f32", 0), (1024, "f32", 1),            # one chunk / four chunks per row
     (32000, "bf16", 0), (32000, "bf16", 1), (32000, "bf16", 3), (32000, "bf16", 7),
     (4096, "bf16", 1), (12296, "bf16", 2), (40000, "f32", 5),
+    # chunk boundaries on 1 KiB multiples (32000 x 2), on 128-byte multiples
+    # (4392 x 2: the 1 KiB rounding would leave a chunk too short), and balanced
+    # (8240 x 3: neither rounding keeps every chunk long enough)
+    (32000, "bf16", 2), (4392, "bf16", 2), (8240, "bf16", 3),
 ])
 def test_tilings(V, dtype, vpt, gpu):
     log(f"tiling V={V} {dtype} vpt={vpt}")
