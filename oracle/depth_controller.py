@@ -21,7 +21,7 @@ What it states, in the paper's order:
   App. D, full-configuration table: p = 0.80, n_min^cov = 8, H_min/H_max = 2/50,
   alpha_ema = 0.30, r_probe = 8, K_warm = 3.
 
-Readings where the paper is silent or ambiguous (each is listed in the design doc):
+Readings where the paper is silent or ambiguous:
   * turn indices are 0-based throughout (the rollout-depth figure states the
     convention; the +1 of the applied cap converts an index to a depth), so a
     successful trajectory of L turns completes at index L - 1 and

@@ -17,7 +17,7 @@ n_traj, kl_mean, kl_m2, kl_var, loss_mass), as the fused call returns them.
                  reliable turn prefix.
   outcome_gap    Sec. 4.2: G_t = K_t^fail - K_t^succ.
 
-Readings where the paper is silent (each is listed in the design doc):
+Readings where the paper is silent:
   * the reliable prefix is the run of leading turns whose survivor count is
     at least n_min = max(floor, ceil(frac * n_traj)); with (8, 0.15) and the
     batch's trajectory count it is the training floor of App. D, with (8,

@@ -9,7 +9,7 @@ The paper trains with a reverse KL on the teacher's top-K support, K = 50
 (App. D: Algorithm 1 computes "top-K reverse-KL token losses"; the
 full-configuration table lists the teacher top-K support size and the
 top-K reverse-KL loss mode).  It does not print the formula.  Reading used
-here (listed in DESIGN.md):
+here:
   * T1  the support S_i of token i is the set of K vocabulary ids the teacher
         ranks highest (passed in by the caller, distinct, in [0, V));
   * T2  both distributions are renormalised over S_i:

@@ -33,7 +33,7 @@ It is a plain, slow, float64 statement of what the hot path computes:
   outcome split   Sec. 4.2: K_t^fail and K_t^succ, the per-turn KL means over
                failed and successful rollouts, whose difference is G_t.
 
-Readings where the paper is silent (each is listed in the design doc):
+Readings where the paper is silent:
   * the loss is over the full vocabulary (the paper trains a top-50 variant);
   * T counts only turns with at least one supervised token; trajectories with
     no supervised token are left out of the mean over trajectories;

@@ -1,7 +1,7 @@
 """Helpers for the GPU parity tests: run the HIP path through the C ABI, run
 the CPU oracle on the same seeded inputs, and compare.
 
-Tolerances (derived in the design doc from the fp32 arithmetic of the kernels):
+Tolerances (derived from the fp32 arithmetic of the kernels):
   * segment table, counts, survivors, status codes: bit-exact;
   * loss (each of L_blend, L_traj, L_turn): relative 1e-4, with an absolute
     floor of 1e-6 (each per-token KL carries ~1e-7 absolute error from the
