@@ -113,6 +113,17 @@ def test_tilings(V, dtype, vpt, gpu):
     check_all(out, ref, mask, 1.0, rows)
 
 
+@pytest.mark.parametrize("dtype", ["bf16", "f32"])
+def test_full_vocabulary_default_tiling(dtype, gpu):
+    """V = 151,936 with the default tiling: 3 chunks (bf16) or 6 chunks (fp32)
+    with 1 KiB-aligned boundaries, every row and gradient checked."""
+    log(f"V=151936 {dtype} default tiling")
+    traj, turn, mask, zs, zt = make_batch(77, n_traj=3, max_turns=4, V=151936, dtype=dtype,
+                                          max_len=12)
+    out, ref, rows = run_both(traj, turn, mask, zs, zt)
+    check_all(out, ref, mask, 1.0, rows)
+
+
 @pytest.mark.parametrize("V,dtype", [(1, "bf16"), (7, "f32"), (24, "bf16"), (1001, "bf16"),
                                      (1003, "f32"), (50257, "bf16"), (8200, "f32")])
 def test_ragged_vocabularies(V, dtype, gpu):

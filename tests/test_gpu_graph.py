@@ -65,3 +65,44 @@ def test_graph_replays_equal_eager(vpt, opts, gpu):
         log(f"graph replays ok (vpt={vpt}, options={opts}): loss={loss_g.tolist()}")
     finally:
         T.set_row_tiling(0)
+
+
+def test_topk_graph_replays_equal_eager(gpu):
+    """The top-K call (support rows, dense zero-fill, scatter) captured in a
+    graph: every replay equals the eager call bit for bit."""
+    w = synth.make("agent")
+    zs_h, zt_h = w.host_logits(0, w.n_tokens)
+    zs, zt = to_device_logits(zs_h), to_device_logits(zt_h)
+    top_v, top_i = torch.topk(zt.float(), 50, dim=1)
+    ids, vals = top_i.to(torch.int32).contiguous(), top_v.contiguous()
+    turn, traj, mask = ids_to_device(w.traj_id, w.turn_id, w.loss_mask)
+    n, V = zs.shape
+    ws = T.TopkWorkspace(n, 50, w.max_turns)
+    grad = torch.empty_like(zs)
+    gk = torch.empty((n, 50), dtype=torch.float32, device=gpu)
+    stats = T.new_turn_stats(w.max_turns)
+    s = torch.cuda.Stream()
+    s.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(s):
+        loss, *_ = T.fwd_bwd_topk(zs, ids, vals, turn, traj, mask, 0.4, grad=grad, grad_topk=gk,
+                                  max_turns=w.max_turns, turn_stats=stats, workspace=ws,
+                                  check=False)
+        s.synchronize()
+        ref = (loss.clone(), grad.clone(), gk.clone(), stats.clone())
+        g = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(g, stream=s):
+            loss_g, *_ = T.fwd_bwd_topk(zs, ids, vals, turn, traj, mask, 0.4, grad=grad,
+                                        grad_topk=gk, max_turns=w.max_turns, turn_stats=stats,
+                                        workspace=ws, check=False)
+    torch.cuda.current_stream().wait_stream(s)
+    for r in range(4):
+        grad.fill_(7)
+        gk.fill_(3)
+        stats.fill_(5)
+        g.replay()
+        torch.cuda.synchronize()
+        assert ws.status() == T.OK
+        assert torch.equal(loss_g, ref[0]), r
+        assert torch.equal(grad.view(torch.int16), ref[1].view(torch.int16)), r
+        assert torch.equal(gk, ref[2]) and torch.equal(stats, ref[3]), r
+    log(f"top-K graph replays ok: loss={loss_g.tolist()}")
