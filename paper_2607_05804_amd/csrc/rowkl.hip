@@ -266,9 +266,10 @@ __device__ inline void merge_chunk(bool offset, const float* w, float rs, float 
 
 // One (row, chunk) task per iteration.  A chunk is the pack range
 // [pack_lo, pack_hi) of the row; thread tid owns packs pack_lo + v * 256 + tid
-// for v < kVpt.  With balanced chunks every pack v < kVpt - 1 lies inside the
-// chunk, so only the last one is predicated (kCheckAll: all of them, for the
-// unaligned scalar path whose chunk sizes are not balanced that way).
+// for v < kVpt.  The host's tiling makes every chunk at least 256 (kVpt - 1)
+// packs long, so every pack v < kVpt - 1 lies inside the chunk and only the
+// last one is predicated (kCheckAll: all of them, for the unaligned scalar
+// path, whose chunks carry no such guarantee).
 template <bool kBf16, int kEpv, int kVpt, bool kCheckAll>
 __global__ __launch_bounds__(kRowThreads) void rowkl_kernel(RowParams p) {
   using P = Pack<kBf16, kEpv>;
