@@ -107,6 +107,9 @@ def check_grad_rows(grad_dev: torch.Tensor, ref: O.Result, grad_scale: float, ro
             continue
         g_ref = ref.grads[r]
         scale = grad_scale * ref.w[r]
+        if scale == 0.0:  # a supervised token of weight 0 (a turn below the support floor)
+            assert np.all(G[k] == 0.0), ("zero-weight row not zero", r)
+            continue
         g_hat = G[k] / scale
         err = np.abs(g_hat - g_ref)
         worst = max(worst, float(err.max()))
