@@ -237,6 +237,33 @@ def options_timing(T, zs, zt, turn, traj, mask, w, grad, steps: int, warmup: int
                     "difference is the cost of the two options"}
 
 
+def graph_timing(T, step, ws, steps: int):
+    """The same call captured once in a HIP graph and replayed: the per-step
+    time without per-launch host overhead (the library's calls enqueue only
+    kernels and never synchronise, so they can be captured)."""
+    import torch
+    s = torch.cuda.Stream()
+    s.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(s):
+        step()
+        g = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(g, stream=s):
+            step()
+        g.replay()
+        s.synchronize()
+        t0 = time.perf_counter()
+        for _ in range(steps):
+            g.replay()
+        s.synchronize()
+        el = time.perf_counter() - t0
+    torch.cuda.current_stream().wait_stream(s)
+    if ws.status() != T.OK:
+        raise RuntimeError(T.status_string(ws.status()))
+    del g
+    return {"ms_per_step": el * 1e3 / steps,
+            "note": "the timed call captured in a HIP graph and replayed; value uses the eager call"}
+
+
 def oracle_topk_timing(w, host):
     """The top-K oracle on the whole batch (CPU baseline of the top-K path)."""
     from oracle import topk_oracle as K
@@ -377,6 +404,7 @@ def main() -> int:
         },
         "step_hbm_gbs": row_bytes / (ms_per_step * 1e-3) / 1e9,
     }
+    out["graph_replay"] = graph_timing(T, step, ws, args.steps)
     out["depth_controller"] = depth_controller_timing(T, stats, w)
     stats_np = T.read_turn_stats(stats)
     out["floor_and_outcome"] = options_timing(T, zs, zt, turn, traj, mask, w, grad, args.steps,
