@@ -124,6 +124,14 @@ def _opts(o):
     (dict(ws_bytes=1024), T.ERR_WORKSPACE),
     (dict(ws=0x500000010), T.ERR_WORKSPACE),
     (dict(max_turns=(2**31 - 2) // 3 + 1), T.ERR_INVALID_ARG),
+    # size limits: 128 chunks per row on the vector path (25 packs of 8 bf16 per
+    # thread) and on the scalar path (32 elements per thread), 32-bit row
+    # strides, token counts and task counts
+    (dict(v=6553600 + 8, ld_s=6553608, ld_t=6553608, ld_g=6553608), T.ERR_INVALID_ARG),
+    (dict(v=1048577, ld_s=1048577, ld_t=1048577, ld_g=1048577), T.ERR_INVALID_ARG),
+    (dict(ld_s=2**31, grad=0), T.ERR_INVALID_ARG),
+    (dict(n=2**31, grad=0), T.ERR_INVALID_ARG),
+    (dict(n=2**24, v=6553600, ld_s=6553600, ld_t=6553600, grad=0), T.ERR_INVALID_ARG),
     # options: floor and fraction ranges; success flags and outcome statistics
     # go together; the outcome statistics must not overlap the turn statistics
     (dict(opts=(-1, 0.0, 0, 0)), T.ERR_INVALID_ARG),

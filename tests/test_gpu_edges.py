@@ -124,6 +124,19 @@ def test_full_vocabulary_default_tiling(dtype, gpu):
     check_all(out, ref, mask, 1.0, rows)
 
 
+@pytest.mark.parametrize("V,dtype", [(6553600, "bf16"), (3276800, "f32"), (1048575, "bf16")])
+def test_vocabularies_at_the_chunk_limit(V, dtype, gpu):
+    """The widest rows the host accepts: 128 chunks per row, on the vector path
+    (25 packs per thread, bf16 and fp32) and on the scalar path (an odd
+    vocabulary, 32 elements per thread); one more pack or element is rejected
+    on the host."""
+    log(f"chunk limit V={V} {dtype}")
+    traj, turn, mask, zs, zt = make_batch(V % 1000, n_traj=2, max_turns=2, V=V, dtype=dtype,
+                                          pad=False, min_len=2, max_len=4)
+    out, ref, rows = run_both(traj, turn, mask, zs, zt, max_turns=2)
+    check_all(out, ref, mask, 1.0, rows)
+
+
 @pytest.mark.parametrize("V,dtype", [(1, "bf16"), (7, "f32"), (24, "bf16"), (1001, "bf16"),
                                      (1003, "f32"), (50257, "bf16"), (8200, "f32")])
 def test_ragged_vocabularies(V, dtype, gpu):
