@@ -112,12 +112,32 @@ typedef struct {
  * [0, max_turns) and of the successful ones' in [max_turns, 2 * max_turns),
  * with the fields and the accumulate_stats rule of turn_stats_out; the two
  * halves partition turn_stats_out's counts and loss mass.
+ *
+ * Per-token outputs (device, caller-owned, or NULL).  Neither may overlap the
+ * logits, the gradient outputs, token_kl_out or each other
+ * (TURNKL_ERR_ALIAS); they are unspecified after a device-detected error.
+ *   token_weight_out  [n_tokens] float: w_i, the weight of token i in
+ *                     L = sum_i w_i KL_i (Sec. 5.2; App. D, Algorithm 1), as
+ *                     described at turnkl_fwd_bwd and above, rounded to float
+ *                     from double; 0 for unsupervised and padding tokens.
+ *   token_lse_out     [n_tokens x 2] float, row-major: for a supervised token
+ *                     the log-partition functions log sum_v exp(zs_i[v]) and
+ *                     log sum_v exp(zt_i[v]) of its student and teacher rows
+ *                     (natural log; Sec. 3, Eq. opd-rkl: log p(v) = z[v] minus
+ *                     this value at temperature 1), so the caller can form
+ *                     log-probabilities without another pass over the rows.
+ *                     On the top-K path the sums run over the token's support
+ *                     S_i (of the student logits and the teacher values).
+ *                     Unsupervised tokens' rows are never read: both entries
+ *                     are NaN.
  */
 typedef struct {
   int32_t support_floor;   /* >= 0; 0 with support_frac 0: no floor */
   double support_frac;     /* in [0, 1] */
   const uint8_t* success;  /* device [n_tokens] outcome flags, or NULL */
   turnkl_turn_stat* outcome_stats_out;  /* device [2 * max_turns], or NULL */
+  float* token_weight_out; /* device [n_tokens], or NULL */
+  float* token_lse_out;    /* device [n_tokens * 2], or NULL */
 } turnkl_options;
 
 /*

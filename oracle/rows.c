@@ -61,12 +61,14 @@ static double log_sum_exp(const double* z, int64_t V) {
  * For each of n_rows rows: zs + r*ld_s and zt + r*ld_t hold V logits.
  *   kl_out[r]           <- KL(p_s || p_t)
  *   g_out + r*ld_g      <- dKL/dz_s (V values), when g_out != NULL
+ *   lse_out[2r], [2r+1] <- lse_s, lse_t (the log-partition functions of the
+ *                          two rows), when lse_out != NULL
  * Rows are independent; they are spread over n_threads OpenMP threads
  * (<= 0: the OpenMP default).  Returns 0, or -1 on a bad argument / OOM.
  */
 int oracle_rows(const void* zs, int64_t ld_s, const void* zt, int64_t ld_t, int dtype,
                 int64_t n_rows, int64_t V, double* kl_out, double* g_out, int64_t ld_g,
-                int n_threads) {
+                double* lse_out, int n_threads) {
   if (!zs || !zt || !kl_out || V < 1 || n_rows < 0 || ld_s < V || ld_t < V) return -1;
   if (dtype < 0 || dtype > 2) return -1;
   if (g_out && ld_g < V) return -1;
@@ -90,6 +92,10 @@ int oracle_rows(const void* zs, int64_t ld_s, const void* zt, int64_t ld_t, int 
     }
     const double lse_s = log_sum_exp(ls, V);
     const double lse_t = log_sum_exp(lt, V);
+    if (lse_out) {
+      lse_out[2 * r] = lse_s;
+      lse_out[2 * r + 1] = lse_t;
+    }
     for (int64_t v = 0; v < V; ++v) {
       ls[v] -= lse_s; /* log p_s(v) */
       lt[v] -= lse_t; /* log p_t(v) */

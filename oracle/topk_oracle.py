@@ -32,6 +32,17 @@ import numpy as np
 from . import turnkl_oracle as O
 
 
+def support_lse(a: np.ndarray, b: np.ndarray) -> np.ndarray:
+    """[n, 2]: log sum_{v in S_i} exp of the student and of the teacher values
+    on each row's support (max shift, then log of the sum), in float64."""
+    a = np.asarray(a, np.float64)
+    b = np.asarray(b, np.float64)
+    ma = a.max(axis=1, keepdims=True)
+    mb = b.max(axis=1, keepdims=True)
+    return np.concatenate([ma + np.log(np.exp(a - ma).sum(axis=1, keepdims=True)),
+                           mb + np.log(np.exp(b - mb).sum(axis=1, keepdims=True))], axis=1)
+
+
 def topk_row_kl(a: np.ndarray, b: np.ndarray, want_grad: bool = True):
     """a, b: float64 [n, K] student and teacher values on each row's support.
     Returns (kl [n], g [n, K]) by the two-pass definition (max shift, lse,
@@ -81,6 +92,7 @@ def fwd_bwd_topk(traj_id, turn_id, loss_mask, alpha: float, max_turns: int, stud
     w0 = O.token_weights(seg, n, loss_mask, 0.0, support_floor, support_frac)
     w1 = O.token_weights(seg, n, loss_mask, 1.0, support_floor, support_frac)
     kl = np.zeros(n, np.float64)
+    lse = np.full((n, 2), np.nan)
     grads = {}
     sup = np.nonzero(loss_mask)[0]
     for k0 in range(0, sup.shape[0], chunk_rows):
@@ -90,8 +102,9 @@ def fwd_bwd_topk(traj_id, turn_id, loss_mask, alpha: float, max_turns: int, stud
         b = np.asarray(teacher_vals[rows], np.float64)
         k_, g = topk_row_kl(a, b)
         kl[rows] = k_
+        lse[rows] = support_lse(a, b)
         for j, r in enumerate(rows.tolist()):
             grads[r] = g[j]
     stats = O.turn_stats([(seg, loss_mask, kl, w)], max_turns)
     return O.Result(O.OK, seg, w, kl, O.losses(w, w0, w1, kl), stats, grads,
-                    O.outcome_split(seg, loss_mask, kl, w, max_turns))
+                    O.outcome_split(seg, loss_mask, kl, w, max_turns), lse)

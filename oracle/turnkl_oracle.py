@@ -96,7 +96,8 @@ def _rows_lib():
         lib.oracle_rows.restype = ctypes.c_int
         lib.oracle_rows.argtypes = [ctypes.c_void_p, ctypes.c_int64, ctypes.c_void_p,
                                     ctypes.c_int64, ctypes.c_int, ctypes.c_int64, ctypes.c_int64,
-                                    ctypes.c_void_p, ctypes.c_void_p, ctypes.c_int64, ctypes.c_int]
+                                    ctypes.c_void_p, ctypes.c_void_p, ctypes.c_int64,
+                                    ctypes.c_void_p, ctypes.c_int]
         lib.oracle_max_threads.restype = ctypes.c_int
         _lib = lib
     return _lib
@@ -244,11 +245,13 @@ def token_weights(seg: Segments, n_tokens: int, loss_mask, alpha: float,
 
 
 def row_kl(zs: np.ndarray, zt: np.ndarray, dtype: int, want_grad: bool = True,
-           n_threads: int = 0):
+           n_threads: int = 0, lse_out: np.ndarray | None = None):
     """KL and dKL/dz_s for each row of [R, V] host arrays.
 
     dtype DTYPE_BF16 takes uint16 bf16 bit patterns, DTYPE_F32 float32 and
-    DTYPE_F64 float64 logits.  Returns (kl [R], g [R, V] or None).
+    DTYPE_F64 float64 logits.  Returns (kl [R], g [R, V] or None); lse_out, a
+    float64 [R, 2] array, receives each row pair's log-partition functions
+    (lse_s, lse_t).
     """
     want = {DTYPE_BF16: np.uint16, DTYPE_F32: np.float32, DTYPE_F64: np.float64}[dtype]
     zs = np.ascontiguousarray(zs, dtype=want) if dtype == DTYPE_F64 else np.ascontiguousarray(zs)
@@ -258,9 +261,12 @@ def row_kl(zs: np.ndarray, zt: np.ndarray, dtype: int, want_grad: bool = True,
     r, v = zs.shape
     kl = np.empty(r, np.float64)
     g = np.empty((r, v), np.float64) if want_grad else None
+    if lse_out is not None:
+        assert lse_out.dtype == np.float64 and lse_out.shape == (r, 2)
+        assert lse_out.flags.c_contiguous
     rc = _rows_lib().oracle_rows(zs.ctypes.data, v, zt.ctypes.data, v, dtype, r, v,
                                  kl.ctypes.data, None if g is None else g.ctypes.data, v,
-                                 n_threads)
+                                 None if lse_out is None else lse_out.ctypes.data, n_threads)
     if rc != 0:
         raise RuntimeError("oracle_rows failed")
     return kl, g
@@ -342,6 +348,7 @@ class Result:
     stats: np.ndarray        # STAT_DTYPE [max_turns]
     grads: dict              # row -> unweighted dKL/dz_s float64 [V]; G = grad_scale * w[row] * g
     outcome_stats: np.ndarray = None  # STAT_DTYPE [2, max_turns]: failed, successful
+    lse: np.ndarray = None   # [N, 2] (lse_s, lse_t) of supervised rows, NaN elsewhere
 
 
 def fwd_bwd(traj_id, turn_id, loss_mask, alpha: float, max_turns: int, row_source,
@@ -367,11 +374,14 @@ def fwd_bwd(traj_id, turn_id, loss_mask, alpha: float, max_turns: int, row_sourc
     w0 = token_weights(seg, n, loss_mask, 0.0, support_floor, support_frac)
     w1 = token_weights(seg, n, loss_mask, 1.0, support_floor, support_frac)
     kl = np.zeros(n, np.float64)
+    lse = np.full((n, 2), np.nan)
     sup = np.nonzero(loss_mask)[0]
     for k0 in range(0, sup.shape[0], chunk_rows):
         rows = sup[k0:k0 + chunk_rows]
         zs, zt = row_source(rows)
-        kl[rows], _ = row_kl(zs, zt, dtype, want_grad=False, n_threads=n_threads)
+        part = np.empty((rows.shape[0], 2))
+        kl[rows], _ = row_kl(zs, zt, dtype, want_grad=False, n_threads=n_threads, lse_out=part)
+        lse[rows] = part
     grads = {}
     want = np.asarray(sorted(set(int(r) for r in grad_rows)), np.int64)
     for k0 in range(0, want.shape[0], chunk_rows):
@@ -382,7 +392,7 @@ def fwd_bwd(traj_id, turn_id, loss_mask, alpha: float, max_turns: int, row_sourc
             grads[r] = g[k]
     stats = turn_stats([(seg, loss_mask, kl, w)], max_turns)
     return Result(OK, seg, w, kl, losses(w, w0, w1, kl), stats, grads,
-                  outcome_split(seg, loss_mask, kl, w, max_turns))
+                  outcome_split(seg, loss_mask, kl, w, max_turns), lse)
 
 
 def outcome_split(seg: Segments, loss_mask, kl, w, max_turns: int):

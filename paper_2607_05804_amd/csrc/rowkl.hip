@@ -335,6 +335,10 @@ __global__ __launch_bounds__(kRowThreads) void rowkl_kernel(RowParams p) {
       valid[v] = (kCheckAll || v == kVpt - 1) ? (v * kRowThreads + tid < n_valid) : true;
 
     if (!p.mask[row]) {
+      if (p.lse && c == 0 && tid == 0) {  // the row is not read: no log-partition function
+        p.lse[2 * row] = __builtin_nanf("");
+        p.lse[2 * row + 1] = __builtin_nanf("");
+      }
       if (p.grad) {
         const typename P::Data z = P::zero();
         const auto rg = chunk_rsrc(static_cast<char*>(p.grad) + (row * p.ld_g + col) * kEs);
@@ -613,8 +617,15 @@ __global__ __launch_bounds__(kRowThreads) void rowkl_kernel(RowParams p) {
 
     // mu = <p_s, (a - b) - (C*_a - C*_b)>,
     // KL = <p_s, a - b> - lse(a) + lse(b) = mu + ((C*_a - R_s) - (C*_b - R_t)) + ln(S_t / S_s)
+    // log sum exp of each row = R + ln S
     const float mu = r.aa / r.ss;
-    if (c == 0 && tid == 0) p.kl[row] = (mu + ((d_s - r_s) - (d_t - r_t))) + kLn2 * log2f(r.st / r.ss);
+    if (c == 0 && tid == 0) {
+      p.kl[row] = (mu + ((d_s - r_s) - (d_t - r_t))) + kLn2 * log2f(r.st / r.ss);
+      if (p.lse) {
+        p.lse[2 * row] = r_s + kLn2 * log2f(r.ss);
+        p.lse[2 * row + 1] = r_t + kLn2 * log2f(r.st);
+      }
+    }
 
     // ---- gradient chunk, straight from registers:
     // G = grad_scale * w * 2^((a - R_s) log2e - log2 S_s) * (((a - b) - (C*_a - C*_b)) - mu),

@@ -53,6 +53,10 @@ __global__ __launch_bounds__(kThreads) void topk_rows(TopkParams p) {
     if (!p.mask[row]) {
       if (p.zero_masked_stage)
         for (int j = lane; j < p.k; j += kWave) stage[j] = 0.0f;
+      if (p.lse && lane == 0) {  // the row is not read: no log-partition function
+        p.lse[2 * row] = __builtin_nanf("");
+        p.lse[2 * row + 1] = __builtin_nanf("");
+      }
       continue;
     }
     float a[kPer], b[kPer];
@@ -107,7 +111,13 @@ __global__ __launch_bounds__(kThreads) void topk_rows(TopkParams p) {
       const int j = lane + q * kWave;
       if (j < p.k) stage[j] = sc * (pr[q] * (d[q] - kl));
     }
-    if (lane == 0) p.kl[row] = kl;
+    if (lane == 0) {
+      p.kl[row] = kl;
+      if (p.lse) {  // log sum exp over the support = max + ln(sum)
+        p.lse[2 * row] = ma + la;
+        p.lse[2 * row + 1] = mb + lb;
+      }
+    }
   }
 }
 

@@ -5,6 +5,8 @@
 #include <math.h>
 #include <string.h>
 
+#include <initializer_list>
+
 #include "turnkl_internal.h"
 
 namespace turnkl {
@@ -100,12 +102,33 @@ size_t matrix_bytes(long long rows, long long ld, long long vocab, size_t es) {
   return rows > 0 ? (size_t)((rows - 1) * ld + vocab) * es : 0;
 }
 
+// A byte range of a caller buffer (p may be null: no range).
+struct Region {
+  const void* p;
+  size_t n;
+};
+
+bool overlaps_any(const void* p, size_t n, std::initializer_list<Region> rs) {
+  for (const Region& r : rs)
+    if (r.p && r.n && overlaps(p, n, r.p, r.n)) return true;
+  return false;
+}
+
+// What the options add to a call besides the segment parameters.
+struct Extras {
+  turnkl_turn_stat* outcome_stats = nullptr;
+  float* weights = nullptr;  // per-token w_i
+  float* lse = nullptr;      // per-token (student, teacher) log-partition functions
+};
+
 // Validates the options shared by both fused entry points and fills the
-// segment parameters they imply.  Returns TURNKL_OK or the error code.
+// segment parameters and outputs they imply.  `taken`: the call's inputs and
+// other outputs, which the per-token outputs must not overlap.  Returns
+// TURNKL_OK or the error code.
 int apply_options(const turnkl_options* o, long long n_tokens, int max_turns,
-                  const turnkl_turn_stat* turn_stats_out, SegParams* sp,
-                  turnkl_turn_stat** outcome_stats_out) {
-  *outcome_stats_out = nullptr;
+                  const turnkl_turn_stat* turn_stats_out, std::initializer_list<Region> taken,
+                  SegParams* sp, Extras* x) {
+  *x = Extras{};
   if (!o) return TURNKL_OK;
   if (o->support_floor < 0) return TURNKL_ERR_INVALID_ARG;
   if (!(o->support_frac >= 0.0 && o->support_frac <= 1.0)) return TURNKL_ERR_INVALID_ARG;
@@ -115,11 +138,30 @@ int apply_options(const turnkl_options* o, long long n_tokens, int max_turns,
       overlaps(o->outcome_stats_out, 2 * (size_t)max_turns * sizeof(turnkl_turn_stat),
                turn_stats_out, (size_t)max_turns * sizeof(turnkl_turn_stat)))
     return TURNKL_ERR_ALIAS;
+  if (((uintptr_t)o->token_weight_out & 3u) != 0 || ((uintptr_t)o->token_lse_out & 3u) != 0)
+    return TURNKL_ERR_INVALID_ARG;
+  if (n_tokens > 0) {
+    const size_t nw = (size_t)n_tokens * 4, nl = (size_t)n_tokens * 8;
+    const size_t nst = (size_t)max_turns * sizeof(turnkl_turn_stat);
+    const Region own[] = {{turn_stats_out, nst}, {o->outcome_stats_out, 2 * nst}};
+    for (const Region& r : own) {
+      if (!r.p) continue;
+      if (o->token_weight_out && overlaps(o->token_weight_out, nw, r.p, r.n)) return TURNKL_ERR_ALIAS;
+      if (o->token_lse_out && overlaps(o->token_lse_out, nl, r.p, r.n)) return TURNKL_ERR_ALIAS;
+    }
+    if (o->token_weight_out && overlaps_any(o->token_weight_out, nw, taken)) return TURNKL_ERR_ALIAS;
+    if (o->token_lse_out && overlaps_any(o->token_lse_out, nl, taken)) return TURNKL_ERR_ALIAS;
+    if (o->token_weight_out && o->token_lse_out &&
+        overlaps(o->token_weight_out, nw, o->token_lse_out, nl))
+      return TURNKL_ERR_ALIAS;
+    x->weights = o->token_weight_out;
+    x->lse = o->token_lse_out;
+  }
   sp->floor_on = o->support_floor > 0 || o->support_frac > 0.0;
   sp->floor = o->support_floor;
   sp->frac = o->support_frac;
   sp->success = o->outcome_stats_out ? o->success : nullptr;
-  *outcome_stats_out = o->outcome_stats_out;
+  x->outcome_stats = o->outcome_stats_out;
   return TURNKL_OK;
 }
 
@@ -163,10 +205,10 @@ int turnkl_fwd_bwd(const void* student_logits, int64_t ld_student, const void* t
   if (((uintptr_t)workspace & 255u) != 0) return TURNKL_ERR_WORKSPACE;
 
   const size_t es = dtype == TURNKL_BF16 ? 2 : 4;
+  const size_t ns = matrix_bytes(n_tokens, ld_student, vocab, es);
+  const size_t nt = matrix_bytes(n_tokens, ld_teacher, vocab, es);
+  const size_t ng = grad_out ? matrix_bytes(n_tokens, ld_grad, vocab, es) : 0;
   if (grad_out && n_tokens > 0) {
-    const size_t ng = matrix_bytes(n_tokens, ld_grad, vocab, es);
-    const size_t ns = matrix_bytes(n_tokens, ld_student, vocab, es);
-    const size_t nt = matrix_bytes(n_tokens, ld_teacher, vocab, es);
     if (overlaps(grad_out, ng, teacher_logits, nt)) return TURNKL_ERR_ALIAS;
     const bool in_place = grad_out == student_logits && ld_grad == ld_student;
     if (!in_place && overlaps(grad_out, ng, student_logits, ns)) return TURNKL_ERR_ALIAS;
@@ -179,7 +221,6 @@ int turnkl_fwd_bwd(const void* student_logits, int64_t ld_student, const void* t
     bool ok = vocab % epv == 0 && ld_student % epv == 0 && ld_teacher % epv == 0;
     ok = ok && ((uintptr_t)student_logits & 15u) == 0 && ((uintptr_t)teacher_logits & 15u) == 0;
     if (grad_out) ok = ok && ld_grad % epv == 0 && ((uintptr_t)grad_out & 15u) == 0;
-    const long long packs = vocab / epv;
     ok = ok && tiling.min_chunk >= (long long)kRowThreads * (tiling.vpt - 1);
     if (!ok) tiling = scalar_tiling(vocab);
   }
@@ -191,13 +232,17 @@ int turnkl_fwd_bwd(const void* student_logits, int64_t ld_student, const void* t
     return TURNKL_ERR_INVALID_ARG;
 
   SegParams sp{traj_id, turn_id, loss_mask, nullptr, (long long)n_tokens, max_turns, 0, 0, 0.0};
-  turnkl_turn_stat* outcome_stats = nullptr;
-  if (int rc = apply_options(options, n_tokens, max_turns, turn_stats_out, &sp, &outcome_stats))
+  Extras ex;
+  if (int rc = apply_options(options, n_tokens, max_turns, turn_stats_out,
+                             {{student_logits, ns}, {teacher_logits, nt}, {grad_out, ng},
+                              {token_kl_out, (size_t)n_tokens * 4}, {loss_out, 3 * sizeof(float)}},
+                             &sp, &ex))
     return rc;
 
   const Layout L = make_layout(n_tokens, workspace_chunks(vocab, dtype), 0, max_turns);
   if (workspace_bytes < L.total) return TURNKL_ERR_WORKSPACE;
-  const Ws ws = bind(workspace, L);
+  Ws ws = bind(workspace, L);
+  if (ex.weights) ws.w = ex.weights;
   float* kl = token_kl_out ? token_kl_out : ws.kl;
 
   // ---- launches
@@ -222,13 +267,14 @@ int turnkl_fwd_bwd(const void* student_logits, int64_t ld_student, const void* t
   rp.n_chunks = tiling.n_chunks;
   rp.align = tiling.align;
   rp.bf16 = dtype == TURNKL_BF16;
+  rp.lse = ex.lse;
   const bool prof = t_row_before && t_row_after;
   if (prof && hipEventRecord(t_row_before, stream) != hipSuccess) return TURNKL_ERR_HIP;
   if (launch_rows(rp, tiling, stream) != hipSuccess) return TURNKL_ERR_HIP;
   if (prof && hipEventRecord(t_row_after, stream) != hipSuccess) return TURNKL_ERR_HIP;
 
-  if (launch_reduce(sp, ws, kl, alpha, loss_out, turn_stats_out, outcome_stats, accumulate_stats,
-                    stream) != hipSuccess)
+  if (launch_reduce(sp, ws, kl, alpha, loss_out, turn_stats_out, ex.outcome_stats,
+                    accumulate_stats, stream) != hipSuccess)
     return TURNKL_ERR_HIP;
   return TURNKL_OK;
 }
@@ -266,34 +312,37 @@ int turnkl_fwd_bwd_topk(const void* student_logits, int64_t ld_student, int dtyp
     if (grad_topk_out && ld_grad_topk < k) return TURNKL_ERR_INVALID_ARG;
   }
   if (((uintptr_t)workspace & 255u) != 0) return TURNKL_ERR_WORKSPACE;
+  const size_t nid = matrix_bytes(n_tokens, ld_topk, k, 4);
+  const size_t ns = matrix_bytes(n_tokens, ld_student, vocab, es);
+  const size_t ng = grad_out ? matrix_bytes(n_tokens, ld_grad, vocab, es) : 0;
+  const size_t ngk = grad_topk_out ? matrix_bytes(n_tokens, ld_grad_topk, k, 4) : 0;
   if (n_tokens > 0) {
-    const size_t nid = matrix_bytes(n_tokens, ld_topk, k, 4);
     if (grad_out) {
-      const size_t ng = matrix_bytes(n_tokens, ld_grad, vocab, es);
-      const size_t ns = matrix_bytes(n_tokens, ld_student, vocab, es);
       if (overlaps(grad_out, ng, teacher_ids, nid) || overlaps(grad_out, ng, teacher_vals, nid))
         return TURNKL_ERR_ALIAS;
       const bool in_place = grad_out == student_logits && ld_grad == ld_student;
       if (!in_place && overlaps(grad_out, ng, student_logits, ns)) return TURNKL_ERR_ALIAS;
-      if (grad_topk_out &&
-          overlaps(grad_out, ng, grad_topk_out, matrix_bytes(n_tokens, ld_grad_topk, k, 4)))
-        return TURNKL_ERR_ALIAS;
+      if (grad_topk_out && overlaps(grad_out, ng, grad_topk_out, ngk)) return TURNKL_ERR_ALIAS;
     }
     if (grad_topk_out) {
-      const size_t nt = matrix_bytes(n_tokens, ld_grad_topk, k, 4);
-      const size_t ns = matrix_bytes(n_tokens, ld_student, vocab, es);
-      if (overlaps(grad_topk_out, nt, teacher_ids, nid) || overlaps(grad_topk_out, nt, teacher_vals, nid) ||
-          overlaps(grad_topk_out, nt, student_logits, ns))
+      if (overlaps(grad_topk_out, ngk, teacher_ids, nid) ||
+          overlaps(grad_topk_out, ngk, teacher_vals, nid) ||
+          overlaps(grad_topk_out, ngk, student_logits, ns))
         return TURNKL_ERR_ALIAS;
     }
   }
   SegParams sp{traj_id, turn_id, loss_mask, nullptr, (long long)n_tokens, max_turns, 0, 0, 0.0};
-  turnkl_turn_stat* outcome_stats = nullptr;
-  if (int rc = apply_options(options, n_tokens, max_turns, turn_stats_out, &sp, &outcome_stats))
+  Extras ex;
+  if (int rc = apply_options(options, n_tokens, max_turns, turn_stats_out,
+                             {{student_logits, ns}, {teacher_ids, nid}, {teacher_vals, nid},
+                              {grad_out, ng}, {grad_topk_out, ngk},
+                              {token_kl_out, (size_t)n_tokens * 4}, {loss_out, 3 * sizeof(float)}},
+                             &sp, &ex))
     return rc;
   const Layout L = make_layout(n_tokens, 0, k, max_turns);
   if (workspace_bytes < L.total) return TURNKL_ERR_WORKSPACE;
-  const Ws ws = bind(workspace, L);
+  Ws ws = bind(workspace, L);
+  if (ex.weights) ws.w = ex.weights;
   float* kl = token_kl_out ? token_kl_out : ws.kl;
 
   // ---- launches
@@ -318,13 +367,14 @@ int turnkl_fwd_bwd_topk(const void* student_logits, int64_t ld_student, int dtyp
   tp.k = k;
   tp.bf16 = dtype == TURNKL_BF16;
   tp.zero_masked_stage = grad_topk_out != nullptr;
+  tp.lse = ex.lse;
   const bool prof = t_row_before && t_row_after;
   if (prof && hipEventRecord(t_row_before, stream) != hipSuccess) return TURNKL_ERR_HIP;
   if (launch_topk_rows(tp, stream) != hipSuccess) return TURNKL_ERR_HIP;
   if (launch_topk_dense(tp, stream) != hipSuccess) return TURNKL_ERR_HIP;
   if (prof && hipEventRecord(t_row_after, stream) != hipSuccess) return TURNKL_ERR_HIP;
-  if (launch_reduce(sp, ws, kl, alpha, loss_out, turn_stats_out, outcome_stats, accumulate_stats,
-                    stream) != hipSuccess)
+  if (launch_reduce(sp, ws, kl, alpha, loss_out, turn_stats_out, ex.outcome_stats,
+                    accumulate_stats, stream) != hipSuccess)
     return TURNKL_ERR_HIP;
   return TURNKL_OK;
 }

@@ -276,6 +276,7 @@ struct RowParams {
   int n_chunks;  // <= kMaxChunks
   int align;     // chunk boundary alignment in packs (chunk_start)
   int bf16;
+  float* lse;    // [n_rows][2] log-partition functions of both rows, or null
 };
 
 hipError_t launch_rows(const RowParams& p, const RowTiling& t, hipStream_t s);
@@ -303,6 +304,7 @@ struct TopkParams {
   int k;
   int bf16;
   int zero_masked_stage;  // write zeros to stage rows of unsupervised tokens
+  float* lse;             // [n_rows][2] log-partition functions on the support, or null
 };
 
 constexpr int kMaxTopK = 1024;

@@ -50,7 +50,8 @@ _lib = None
 class Options(ctypes.Structure):
     """turnkl_options (include/turnkl.h)."""
     _fields_ = [("support_floor", ctypes.c_int32), ("support_frac", ctypes.c_double),
-                ("success", ctypes.c_void_p), ("outcome_stats_out", ctypes.c_void_p)]
+                ("success", ctypes.c_void_p), ("outcome_stats_out", ctypes.c_void_p),
+                ("token_weight_out", ctypes.c_void_p), ("token_lse_out", ctypes.c_void_p)]
 
 
 class DepthConfig(ctypes.Structure):
@@ -168,14 +169,20 @@ def profile_row_kernel(before, after) -> None:
     lib().turnkl_profile_row_kernel(b, a)
 
 
-def _options(n: int, support_floor: int, support_frac: float, success, outcome_stats):
+def _options(n: int, support_floor: int, support_frac: float, success, outcome_stats,
+             token_weights=None, token_lse=None):
     """turnkl_options for the keyword arguments, or None when all are off."""
-    if not support_floor and not support_frac and success is None and outcome_stats is None:
+    if (not support_floor and not support_frac and success is None and outcome_stats is None
+            and token_weights is None and token_lse is None):
         return None
     if success is not None and (success.dtype != torch.uint8 or success.numel() != n):
         raise ValueError("success must be uint8 with one entry per row")
+    for t, per, name in ((token_weights, 1, "token_weights"), (token_lse, 2, "token_lse")):
+        if t is not None and (t.dtype != torch.float32 or t.numel() != per * n
+                              or not t.is_contiguous()):
+            raise ValueError(f"{name} must be a contiguous float32 tensor of {per} x n_tokens")
     return ctypes.byref(Options(int(support_floor), float(support_frac), _ptr(success),
-                                _ptr(outcome_stats)))
+                                _ptr(outcome_stats), _ptr(token_weights), _ptr(token_lse)))
 
 
 def _dtype_code(t: torch.Tensor) -> int:
@@ -232,7 +239,8 @@ def fwd_bwd(student: torch.Tensor, teacher: torch.Tensor, turn_id: torch.Tensor,
             accumulate_stats: bool = False, token_kl: bool | torch.Tensor = False,
             workspace: Workspace | None = None, check: bool = True, support_floor: int = 0,
             support_frac: float = 0.0, success: torch.Tensor | None = None,
-            outcome_stats: torch.Tensor | None = None):
+            outcome_stats: torch.Tensor | None = None, token_weights: torch.Tensor | None = None,
+            token_lse: torch.Tensor | None = None):
     """One fused forward + backward call on the current stream.
 
     grad: "new" allocates the gradient, "inplace" writes it over `student`,
@@ -242,8 +250,11 @@ def fwd_bwd(student: torch.Tensor, teacher: torch.Tensor, turn_id: torch.Tensor,
     merges into it.  support_floor / support_frac: the turn-support floor of
     the turn term; success (uint8 per token) with outcome_stats (a
     new_turn_stats(2 * max_turns) buffer: failed, then successful): the
-    per-outcome statistics (turnkl_options).  Returns (loss[3] tensor, grad or
-    None, turn_stats or None, token_kl or None, workspace).
+    per-outcome statistics (turnkl_options).  token_weights (float32 [N]) and
+    token_lse (float32 [N, 2]) receive each token's weight w_i and the
+    log-partition functions of its student and teacher rows (NaN for
+    unsupervised tokens).  Returns (loss[3] tensor, grad or None, turn_stats or
+    None, token_kl or None, workspace).
     """
     dt = _dtype_code(student)
     if teacher.dtype != student.dtype:
@@ -278,7 +289,8 @@ def fwd_bwd(student: torch.Tensor, teacher: torch.Tensor, turn_id: torch.Tensor,
         float(alpha), float(grad_scale), _ptr(loss), _ptr(grad_t),
         (_row_stride(grad_t) if n else v) if grad_t is not None else 0, _ptr(turn_stats),
         int(max_turns), int(bool(accumulate_stats)), _ptr(kl_t),
-        _options(n, support_floor, support_frac, success, outcome_stats), _ptr(workspace.tensor),
+        _options(n, support_floor, support_frac, success, outcome_stats, token_weights, token_lse),
+        _ptr(workspace.tensor),
         workspace.nbytes, ctypes.c_void_p(stream))
     if rc != OK:
         raise TurnKLError(rc, "turnkl_fwd_bwd")
@@ -309,13 +321,15 @@ def fwd_bwd_topk(student: torch.Tensor, teacher_ids: torch.Tensor, teacher_vals:
                  accumulate_stats: bool = False, token_kl: bool | torch.Tensor = False,
                  workspace: TopkWorkspace | None = None, check: bool = True,
                  support_floor: int = 0, support_frac: float = 0.0,
-                 success: torch.Tensor | None = None, outcome_stats: torch.Tensor | None = None):
+                 success: torch.Tensor | None = None, outcome_stats: torch.Tensor | None = None,
+                 token_weights: torch.Tensor | None = None, token_lse: torch.Tensor | None = None):
     """The top-K variant (turnkl_fwd_bwd_topk) on the current stream.
 
     teacher_ids: int32 [N, K]; teacher_vals: float32 [N, K].  grad as in
     fwd_bwd (dense, zero off the support); grad_topk: True allocates, or a
     float32 [N, K] tensor receives, the gradient on the support; the options
-    as in fwd_bwd.  Returns
+    as in fwd_bwd (token_lse: log-partition functions over each token's
+    support).  Returns
     (loss[3], grad or None, grad_topk or None, turn_stats or None,
     token_kl or None, workspace).
     """
@@ -363,7 +377,8 @@ def fwd_bwd_topk(student: torch.Tensor, teacher_ids: torch.Tensor, teacher_vals:
         (_row_stride(grad_t) if n else v) if grad_t is not None else 0, _ptr(gk),
         (int(gk.stride(0)) if n else k) if gk is not None else 0, _ptr(turn_stats),
         int(max_turns), int(bool(accumulate_stats)), _ptr(kl_t),
-        _options(n, support_floor, support_frac, success, outcome_stats), _ptr(workspace.tensor),
+        _options(n, support_floor, support_frac, success, outcome_stats, token_weights, token_lse),
+        _ptr(workspace.tensor),
         workspace.nbytes, ctypes.c_void_p(stream))
     if rc != OK:
         raise TurnKLError(rc, "turnkl_fwd_bwd_topk")

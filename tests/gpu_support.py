@@ -80,6 +80,30 @@ def check_token_kl(kl_dev: torch.Tensor, ref_kl: np.ndarray, mask: np.ndarray) -
     assert np.all(got[np.asarray(mask) == 0] == 0.0)
 
 
+def check_token_weights(w_dev: torch.Tensor, ref_w: np.ndarray, mask: np.ndarray) -> None:
+    """w_i is the fp64 weight rounded to float: within one float rounding of
+    the oracle's value, exactly 0 for unsupervised tokens."""
+    got = w_dev.cpu().numpy()[: ref_w.shape[0]].astype(np.float64)
+    err = np.abs(got - ref_w)
+    bad = np.nonzero(err > 2.0 ** -23 * np.abs(ref_w))[0]
+    assert bad.size == 0, (bad[:5], got[bad[:5]], ref_w[bad[:5]])
+    assert np.all(got[np.asarray(mask) == 0] == 0.0)
+
+
+def check_token_lse(lse_dev: torch.Tensor, ref_lse: np.ndarray, mask: np.ndarray) -> None:
+    """Log-partition functions of supervised rows within 2e-5 + 1e-6 |lse| of
+    the oracle's float64 values (float references and sums); NaN for
+    unsupervised rows, which are never read."""
+    n = ref_lse.shape[0]
+    got = lse_dev.reshape(-1)[: 2 * n].reshape(n, 2).cpu().numpy().astype(np.float64)
+    sup = np.asarray(mask)[:n] != 0
+    assert np.all(np.isnan(got[~sup]))
+    err = np.abs(got[sup] - ref_lse[sup])
+    bound = 2e-5 + 1e-6 * np.abs(ref_lse[sup])
+    bad = np.argwhere(err > bound)
+    assert bad.size == 0, (bad[:5], got[sup][tuple(bad[:5].T)], ref_lse[sup][tuple(bad[:5].T)])
+
+
 def check_stats(stats_buf: torch.Tensor, ref: np.ndarray) -> None:
     got = T.read_turn_stats(stats_buf)
     assert np.array_equal(got["n_tokens"], ref["n_tokens"])

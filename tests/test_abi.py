@@ -88,10 +88,13 @@ def _call(**kw):
 
 
 def _opts(o):
-    """(support_floor, support_frac, success, outcome_stats_out) -> turnkl_options*."""
+    """(support_floor, support_frac, success, outcome_stats_out[, token_weight_out,
+    token_lse_out]) -> turnkl_options*."""
     if o is None:
         return None
-    return ctypes.byref(T.Options(o[0], o[1], o[2] or None, o[3] or None))
+    o = tuple(o) + (0,) * (6 - len(o))
+    return ctypes.byref(T.Options(o[0], o[1], o[2] or None, o[3] or None, o[4] or None,
+                                  o[5] or None))
 
 
 @pytest.mark.parametrize("kw,code", [
@@ -142,6 +145,18 @@ def _opts(o):
     (dict(opts=(0, 0.0, 0, 0x710000000)), T.ERR_INVALID_ARG),
     (dict(stats=0x710000000, opts=(0, 0.0, 0x700000000, 0x710000000 + 48 * 7)), T.ERR_ALIAS),
     (dict(stats=0x710000000 + 48 * 15, opts=(0, 0.0, 0x700000000, 0x710000000)), T.ERR_ALIAS),
+    # per-token outputs: 4-byte aligned, overlapping no input, no other output
+    # and not each other
+    (dict(opts=(0, 0.0, 0, 0, 0x720000002, 0)), T.ERR_INVALID_ARG),
+    (dict(opts=(0, 0.0, 0, 0, 0, 0x730000001)), T.ERR_INVALID_ARG),
+    (dict(opts=(0, 0.0, 0, 0, 0x100000000 + 4096, 0)), T.ERR_ALIAS),
+    (dict(opts=(0, 0.0, 0, 0, 0, 0x200000000 + 8)), T.ERR_ALIAS),
+    (dict(opts=(0, 0.0, 0, 0, 0x400000000, 0)), T.ERR_ALIAS),
+    (dict(kl=0x720000000, opts=(0, 0.0, 0, 0, 0, 0x720000000 + 4 * 63)), T.ERR_ALIAS),
+    (dict(opts=(0, 0.0, 0, 0, 0x720000000, 0x720000000 + 4 * 63)), T.ERR_ALIAS),
+    (dict(opts=(0, 0.0, 0, 0, 0x300300000 + 8, 0)), T.ERR_ALIAS),
+    (dict(stats=0x710000000, opts=(0, 0.0, 0, 0, 0, 0x710000000 + 48 * 7)), T.ERR_ALIAS),
+    (dict(opts=(0, 0.0, 0x700000000, 0x710000000, 0x710000000 + 48 * 15, 0)), T.ERR_ALIAS),
 ])
 def test_host_rejects_bad_arguments_before_launch(kw, code):
     assert _call(**kw) == code
@@ -202,6 +217,12 @@ def test_topk_workspace_bytes():
     (dict(ws_bytes=1024), T.ERR_WORKSPACE),
     (dict(opts=(-3, 0.0, 0, 0)), T.ERR_INVALID_ARG),
     (dict(opts=(0, 0.0, 0x700000000, 0)), T.ERR_INVALID_ARG),
+    # per-token outputs overlapping the support, the sparse gradient or each other
+    (dict(opts=(0, 0.0, 0, 0, 0x200000000 + 64, 0)), T.ERR_ALIAS),
+    (dict(opts=(0, 0.0, 0, 0, 0, 0x210000000 + 8)), T.ERR_ALIAS),
+    (dict(opts=(0, 0.0, 0, 0, 0x600000000 + 200, 0)), T.ERR_ALIAS),
+    (dict(opts=(0, 0.0, 0, 0, 0x720000000, 0x720000000 + 4 * 63)), T.ERR_ALIAS),
+    (dict(opts=(0, 0.0, 0, 0, 0x720000001, 0)), T.ERR_INVALID_ARG),
 ])
 def test_topk_host_rejects_bad_arguments_before_launch(kw, code):
     assert _call_topk(**kw) == code

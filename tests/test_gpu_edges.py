@@ -5,7 +5,8 @@ import pytest
 import torch
 
 from gpu_support import (check_grad_rows, check_loss, check_segments, check_stats,
-                         check_token_kl, ids_to_device, log, to_device_logits)
+                         check_token_kl, check_token_lse, check_token_weights, ids_to_device, log,
+                         to_device_logits)
 from oracle import turnkl_oracle as O
 from paper_2607_05804_amd import turnkl as T
 
@@ -171,6 +172,55 @@ def test_grad_scale(grad_scale, gpu):
         assert torch.count_nonzero(out[1].float()).item() == 0
     else:
         check_all(out, ref, mask, grad_scale, rows)
+
+
+@pytest.mark.parametrize("V,dtype,vpt,shift,grad,floor", [
+    (32000, "bf16", 3, 0.0, "new", 2),      # six chunks per row, support floor
+    (151936, "bf16", 0, 0.0, "inplace", 0),  # three 1 KiB-aligned chunks, in place
+    (1001, "f32", 0, 0.0, None, 0),          # scalar path, forward only
+    (4096, "f32", 0, 5000.0, "new", 0),      # offset chunks (|logits| > 64)
+    (8240, "bf16", 3, -96.0, "new", 8),      # balanced chunks, offset rows, floor
+])
+def test_per_token_weights_and_log_partition_functions(V, dtype, vpt, shift, grad, floor, gpu):
+    """The optional per-token outputs: w_i and both rows' log-partition
+    functions (NaN for unsupervised rows), against the oracle; the other
+    outputs are unchanged by asking for them."""
+    log(f"per-token outputs V={V} {dtype} vpt={vpt} shift={shift} grad={grad} floor={floor}")
+    traj, turn, mask, zs_h, zt_h = make_batch(300 + V % 97, n_traj=4, max_turns=5, V=V,
+                                              dtype="f32", max_len=12)
+    zs_h, zt_h = _as(dtype, zs_h + shift), _as(dtype, zt_h + shift * 0.5)
+    n = len(traj)
+    zs_copy, zt = to_device_logits(zs_h), to_device_logits(zt_h)
+    turn_d, traj_d, mask_d = ids_to_device(traj, turn, mask)
+    wts = torch.full((n,), float("nan"), dtype=torch.float32, device="cuda")
+    lse = torch.zeros((n, 2), dtype=torch.float32, device="cuda")
+    outs = []
+    T.set_row_tiling(vpt)
+    try:
+        for extra in (dict(token_weights=wts, token_lse=lse), {}):
+            stats = T.new_turn_stats(5)
+            src = zs_copy.clone()
+            loss, g, _, kl, ws = T.fwd_bwd(src, zt, turn_d, traj_d, mask_d, 0.4, grad=grad,
+                                           max_turns=5, turn_stats=stats, token_kl=True,
+                                           support_floor=floor, **extra)
+            torch.cuda.synchronize()
+            outs.append((loss.cpu(), None if g is None else g.cpu(), stats.cpu(), kl.cpu()))
+    finally:
+        T.set_row_tiling(0)
+    ref = O.fwd_bwd(traj, turn, mask, 0.4, 5, lambda r: (zs_h[r], zt_h[r]),
+                    O.DTYPE_BF16 if dtype == "bf16" else O.DTYPE_F32, 1.0,
+                    list(range(n)), support_floor=floor)
+    check_token_weights(wts, ref.w, mask)
+    check_token_lse(lse, ref.lse, mask)
+    check_loss(outs[0][0], ref.loss)
+    check_token_kl(outs[0][3], ref.kl, mask)
+    if grad is not None:
+        check_grad_rows(outs[0][1], ref, 1.0, list(range(n)), mask)
+    # bit-identical with and without the extra outputs
+    for a, b in zip(outs[0], outs[1]):
+        if a is not None:
+            assert torch.equal(a.view(torch.uint8) if a.dtype == torch.bfloat16 else a,
+                               b.view(torch.uint8) if b.dtype == torch.bfloat16 else b)
 
 
 def test_forward_only(gpu):

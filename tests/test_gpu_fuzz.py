@@ -1,13 +1,15 @@
 """Seeded random configurations of the fused call against the oracle: vocabulary
 (vector and scalar paths), dtype, tiling, padded row stride, alpha, the sign
 and size of grad_scale, in-place gradient, turn-support floor and outcome
-split, all at once.  Every row, gradient and statistic is compared."""
+split, and the optional per-token weights and log-partition functions, all at
+once.  Every row, gradient and statistic is compared."""
 import numpy as np
 import pytest
 import torch
 
 from gpu_support import (check_grad_rows, check_loss, check_segments, check_stats,
-                         check_token_kl, ids_to_device, log, to_device_logits)
+                         check_token_kl, check_token_lse, check_token_weights, ids_to_device, log,
+                         to_device_logits)
 from oracle import turnkl_oracle as O
 from paper_2607_05804_amd import turnkl as T
 from test_gpu_edges import make_batch
@@ -31,9 +33,10 @@ def _case(k):
     outcome = rng.uniform() < 0.5
     n_traj = int(rng.integers(1, 9))
     max_turns = int(rng.integers(1, 9))
+    per_token = rng.uniform() < 0.5
     return dict(seed=6000 + k, dtype=dtype, V=V, vpt=vpt, ld=ld, alpha=alpha,
                 grad_scale=grad_scale, in_place=in_place, floor=floor, frac=frac,
-                outcome=outcome, n_traj=n_traj, max_turns=max_turns)
+                outcome=outcome, n_traj=n_traj, max_turns=max_turns, per_token=per_token)
 
 
 def _device(h, ld):
@@ -63,13 +66,18 @@ def test_random_configuration(k, gpu):
     turn_d, traj_d, mask_d = ids_to_device(traj, turn, mask)
     stats = T.new_turn_stats(c["max_turns"])
     ostats = T.new_turn_stats(2 * c["max_turns"]) if succ is not None else None
+    extra = {}
+    if c["per_token"]:
+        extra = dict(token_weights=torch.empty(n, dtype=torch.float32, device="cuda"),
+                     token_lse=torch.empty((n, 2), dtype=torch.float32, device="cuda"))
     T.set_row_tiling(c["vpt"])
     try:
         loss, g, _, kl, ws = T.fwd_bwd(
             zs, zt, turn_d, traj_d, mask_d, c["alpha"], grad_scale=c["grad_scale"],
             grad="inplace" if c["in_place"] else "new", max_turns=c["max_turns"],
             turn_stats=stats, token_kl=True, support_floor=c["floor"], support_frac=c["frac"],
-            success=None if succ is None else torch.from_numpy(succ).cuda(), outcome_stats=ostats)
+            success=None if succ is None else torch.from_numpy(succ).cuda(), outcome_stats=ostats,
+            **extra)
     finally:
         T.set_row_tiling(0)
     torch.cuda.synchronize()
@@ -87,6 +95,9 @@ def test_random_configuration(k, gpu):
         half = 48 * c["max_turns"]
         check_stats(ostats[:half], ref.outcome_stats[0])
         check_stats(ostats[half:], ref.outcome_stats[1])
+    if extra:
+        check_token_weights(extra["token_weights"], ref.w, mask)
+        check_token_lse(extra["token_lse"], ref.lse, mask)
     if c["in_place"]:
         assert g.data_ptr() == zs.data_ptr()
     check_grad_rows(g, ref, c["grad_scale"], rows, mask)

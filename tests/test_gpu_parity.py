@@ -14,7 +14,7 @@ import torch
 
 import synth
 from gpu_support import (check_grad_rows, check_loss, check_segments, check_stats,
-                         check_token_kl, device_row_source, ids_to_device, log, oracle_dtype,
+                         check_token_kl, check_token_lse, check_token_weights, device_row_source, ids_to_device, log, oracle_dtype,
                          sample_rows, to_device_logits)
 from oracle import turnkl_oracle as O
 from paper_2607_05804_amd import turnkl as T
@@ -22,12 +22,12 @@ from paper_2607_05804_amd import turnkl as T
 pytestmark = pytest.mark.gpu
 
 
-def _run(zs, zt, w, alpha, grad_scale, grad="new", ws=None):
+def _run(zs, zt, w, alpha, grad_scale, grad="new", ws=None, **extra):
     turn, traj, mask = ids_to_device(w.traj_id, w.turn_id, w.loss_mask)
     stats = T.new_turn_stats(w.max_turns)
     loss, g, _, kl, ws = T.fwd_bwd(zs, zt, turn, traj, mask, alpha, grad_scale=grad_scale,
                                    grad=grad, max_turns=w.max_turns, turn_stats=stats,
-                                   token_kl=True, workspace=ws)
+                                   token_kl=True, workspace=ws, **extra)
     torch.cuda.synchronize()
     return loss, g, stats, kl, ws
 
@@ -70,8 +70,15 @@ def _full_size(name, gpu, check_alphas=None):
     for k, alpha in enumerate(alphas):
         last = k == len(alphas) - 1
         grad = "inplace" if (w.in_place and last) else "new"
-        loss, g, stats, kl, ws = _run(zs, zt, w, alpha, 1.0, grad=grad, ws=ws)
+        # the first call also returns the per-token weights and log-partition functions
+        extra = {} if k else dict(
+            token_weights=torch.empty(w.n_tokens, dtype=torch.float32, device=gpu),
+            token_lse=torch.empty((w.n_tokens, 2), dtype=torch.float32, device=gpu))
+        loss, g, stats, kl, ws = _run(zs, zt, w, alpha, 1.0, grad=grad, ws=ws, **extra)
         w_a = O.token_weights(ref.seg, w.n_tokens, w.loss_mask, alpha)
+        if extra:
+            check_token_weights(extra["token_weights"], w_a, w.loss_mask)
+            check_token_lse(extra["token_lse"], ref.lse, w.loss_mask)
         w0 = O.token_weights(ref.seg, w.n_tokens, w.loss_mask, 0.0)
         w1 = O.token_weights(ref.seg, w.n_tokens, w.loss_mask, 1.0)
         ref_loss = O.losses(w_a, w0, w1, ref.kl)

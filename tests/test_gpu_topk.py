@@ -6,7 +6,8 @@ import pytest
 import torch
 
 import synth
-from gpu_support import (check_loss, check_segments, check_stats, check_token_kl, ids_to_device,
+from gpu_support import (check_loss, check_segments, check_stats, check_token_kl,
+                         check_token_lse, check_token_weights, ids_to_device,
                          log, rows_to_host, sample_rows, to_device_logits)
 from oracle import topk_oracle as K
 from oracle import turnkl_oracle as O
@@ -103,6 +104,41 @@ def test_topk_in_place_forward_only_and_scale(gpu):
                                          grad_topk=False)
     assert g3 is None and gk3 is None
     assert torch.equal(l3, l1) and torch.equal(k3, k1)
+
+
+@pytest.mark.parametrize("dtype,k,floor", [("bf16", 50, 0), ("f32", 7, 2), ("bf16", 200, 8)])
+def test_topk_per_token_weights_and_support_lse(dtype, k, floor, gpu):
+    """The per-token weights and the log-partition functions over each
+    token's support (NaN for unsupervised tokens); asking for them leaves
+    every other output bit-identical."""
+    log(f"topk per-token outputs {dtype} K={k} floor={floor}")
+    traj, turn, mask, zs_h, zt_h = make_batch(80 + k, V=4096, dtype=dtype)
+    ids, vals = _support(_f32(zt_h), k, np.random.default_rng(k))
+    n = len(traj)
+    zs = to_device_logits(zs_h)
+    turn_d, traj_d, mask_d = ids_to_device(traj, turn, mask)
+    ids_d, vals_d = torch.from_numpy(ids).cuda(), torch.from_numpy(vals).cuda()
+    wts = torch.full((n,), float("nan"), dtype=torch.float32, device="cuda")
+    lse = torch.zeros((n, 2), dtype=torch.float32, device="cuda")
+    outs = []
+    for extra in (dict(token_weights=wts, token_lse=lse), {}):
+        o = T.fwd_bwd_topk(zs, ids_d, vals_d, turn_d, traj_d, mask_d, 0.4, grad_topk=True,
+                           max_turns=8, turn_stats=T.new_turn_stats(8), token_kl=True,
+                           support_floor=floor, **extra)
+        torch.cuda.synchronize()
+        outs.append([x.cpu() for x in o[:5]])
+    dt = O.DTYPE_BF16 if dtype == "bf16" else O.DTYPE_F32
+    ref = K.fwd_bwd_topk(traj, turn, mask, 0.4, 8,
+                         lambda rows, i: np.take_along_axis(zs_h[rows], i, axis=1), ids, vals, dt,
+                         support_floor=floor)
+    check_token_weights(wts, ref.w, mask)
+    check_token_lse(lse, ref.lse, mask)
+    check_loss(outs[0][0], ref.loss)
+    check_token_kl(outs[0][4], ref.kl, mask)
+    for a, b in zip(outs[0], outs[1]):
+        a = a.view(torch.int16) if a.dtype == torch.bfloat16 else a
+        b = b.view(torch.int16) if b.dtype == torch.bfloat16 else b
+        assert torch.equal(a, b)
 
 
 def test_topk_identical_values_give_exact_zeros(gpu):
