@@ -168,6 +168,49 @@ def topk_timing(T, zs, zt, turn, traj, mask, w, steps: int, warmup: int, k: int 
     return out, host + (zs_at,)
 
 
+def all_supervised_timing(T, zs, zt, turn, traj, w, grad, steps: int, warmup: int):
+    """The same logits with every token supervised (loss mask all ones): every
+    row reads both logit rows and writes its gradient, 3 V s bytes per token,
+    the row kernel's clean roofline case."""
+    import numpy as np
+    import torch
+    dev = zs.device
+    n, V = zs.shape
+    mask = (traj >= 0).to(torch.uint8)  # every token but padding
+    n_sup = int(mask.sum().item())
+    stats = T.new_turn_stats(w.max_turns, device=dev)
+    ws = T.Workspace(n, V, T.BF16, w.max_turns, device=dev)
+
+    def step():
+        return T.fwd_bwd(zs, zt, turn, traj, mask, w.alphas[0], grad=grad, max_turns=w.max_turns,
+                         turn_stats=stats, workspace=ws, check=False)
+
+    for _ in range(warmup):
+        step()
+    torch.cuda.synchronize()
+    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+          for _ in range(steps)]
+    for a, b in ev:
+        a.record()
+        b.record()
+    torch.cuda.synchronize()
+    for a, b in ev:
+        T.profile_row_kernel(a, b)
+        step()
+    T.profile_row_kernel(None, None)
+    torch.cuda.synchronize()
+    if ws.status() != T.OK:
+        raise RuntimeError(T.status_string(ws.status()))
+    ms = np.array([a.elapsed_time(b) for a, b in ev])
+    by = n_sup * 3 * V * 2 + (n - n_sup) * V * 2
+    del ws
+    return {"tokens": n, "supervised_tokens": n_sup, "algorithmic_bytes_per_launch": by,
+            "kernel_ms_mean": float(ms.mean()), "kernel_ms_median": float(np.median(ms)),
+            "achieved_gbs": by / (ms.mean() * 1e-3) / 1e9,
+            "frac": by / (ms.mean() * 1e-3) / 1e9 / HBM_PEAK_GBS,
+            "note": "same logits with every non-padding token supervised (3 V s bytes per token)"}
+
+
 def options_timing(T, zs, zt, turn, traj, mask, w, grad, steps: int, warmup: int):
     """The fused call with App. D's turn-support floor (8, 0.15) and the
     per-outcome statistics (success flags: the even-numbered trajectories
@@ -298,6 +341,33 @@ def copy_probe(gib: float, steps: int) -> int:
     return 0
 
 
+def sustain(T, step, ws, n_tokens: int, seconds: float) -> int:
+    """The timed call back to back for `seconds` (synchronising every 50
+    calls), with one progress line per second: the steady load under which
+    clocks and power are read."""
+    import torch
+    t0 = time.perf_counter()
+    last = t0
+    calls = 0
+    while time.perf_counter() - t0 < seconds:
+        for _ in range(50):
+            step()
+        torch.cuda.synchronize()
+        calls += 50
+        now = time.perf_counter()
+        if now - last >= 1.0:
+            print(f"sustain: {calls} calls, {now - t0:.1f} s, {(now - t0) * 1e3 / calls:.3f} ms per call",
+                  flush=True)
+            last = now
+    el = time.perf_counter() - t0
+    if ws.status() != T.OK:
+        raise RuntimeError(T.status_string(ws.status()))
+    print(json.dumps({"sustained_s": el, "calls": calls, "ms_per_call": el * 1e3 / calls,
+                      "tokens_per_s": n_tokens * calls / el, "start_unix": time.time() - el,
+                      "end_unix": time.time()}), flush=True)
+    return 0
+
+
 def main() -> int:
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -309,6 +379,10 @@ def main() -> int:
     ap.add_argument("--copy-probe", type=float, default=0.0, metavar="GIB",
                     help="instead of the step, time a plain device copy of this many GiB "
                          "(bandwidth context and counter calibration)")
+    ap.add_argument("--sustain", type=float, default=0.0, metavar="SECONDS",
+                    help="instead of the measurements, run the timed call back to back for "
+                         "this long and report its rate (for clock and power readings under "
+                         "a steady load)")
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py runs on one GPU only (asked for --gpus {args.gpus}); the multi-GPU "
@@ -348,6 +422,8 @@ def main() -> int:
     torch.cuda.synchronize()
     if ws.status() != T.OK:
         raise RuntimeError(T.status_string(ws.status()))
+    if args.sustain > 0:
+        return sustain(T, step, ws, n, args.sustain)
 
     ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
           for _ in range(args.steps)]
@@ -365,7 +441,8 @@ def main() -> int:
     if ws.status() != T.OK:
         raise RuntimeError(T.status_string(ws.status()))
 
-    row_ms = float(np.mean([a.elapsed_time(b) for a, b in ev]))
+    row_all = np.array([a.elapsed_time(b) for a, b in ev])
+    row_ms = float(row_all.mean())
     ms_per_step = elapsed * 1e3 / args.steps
     es = 2
     row_bytes = n_sup * 3 * V * es + (n - n_sup) * V * es
@@ -400,15 +477,21 @@ def main() -> int:
             "traffic": traffic,
             "kernel": "rowkl_kernel",
             "kernel_ms": row_ms,
+            "kernel_ms_median": float(np.median(row_all)),
+            "kernel_ms_p10": float(np.percentile(row_all, 10)),
+            "kernel_ms_p90": float(np.percentile(row_all, 90)),
             "algorithmic_bytes_per_launch": row_bytes,
         },
         "step_hbm_gbs": row_bytes / (ms_per_step * 1e-3) / 1e9,
+        "supervised_tokens_per_s": n_sup * args.steps / elapsed,
     }
     out["graph_replay"] = graph_timing(T, step, ws, args.steps)
     out["depth_controller"] = depth_controller_timing(T, stats, w)
     stats_np = T.read_turn_stats(stats)
     out["floor_and_outcome"] = options_timing(T, zs, zt, turn, traj, mask, w, grad, args.steps,
                                               args.warmup)
+    out["all_supervised"] = all_supervised_timing(T, zs, zt, turn, traj, w, grad, args.steps,
+                                                  args.warmup)
     del grad
     torch.cuda.empty_cache()
     out["topk"], topk_host = topk_timing(T, zs, zt, turn, traj, mask, w, args.steps, args.warmup)

@@ -5,8 +5,9 @@
 //              segment's shares of L_blend = sum_i w_i KL_i (App. D,
 //              Algorithm 1), L_traj (alpha = 0) and L_turn (alpha = 1).
 // finalize     one workgroup per (group, turn index t): the segments of turn t
-//              merged in segment order (pairwise update of Chan, Golub &
-//              LeVeque for the mean and m2) -> pooled mean K_t (Sec. 4.3, Eq.
+//              merged in a fixed order (each thread's segments s, s + 256, ...
+//              in turn, then a fixed tree over the threads; pairwise update of
+//              Chan, Golub & LeVeque for the mean and m2) -> pooled mean K_t (Sec. 4.3, Eq.
 //              observed-turn-kl), population variance, survivors n_t (Sec.
 //              5.1, App. D), loss mass (Sec. 4.4); optionally merged into the
 //              caller's running statistics.  Group 0 takes every trajectory;
