@@ -55,6 +55,18 @@ def committed_traffic():
     return float(t.group(1))
 
 
+def cpu_model() -> str | None:
+    """The host CPU's model name (first processor in /proc/cpuinfo)."""
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return None
+
+
 def cpu_baseline(w, sample_tokens: int):
     """The float64 oracle, timed on a prefix of the batch (all its rows,
     loss, gradient of every supervised row and per-turn stats)."""
@@ -72,6 +84,7 @@ def cpu_baseline(w, sample_tokens: int):
     dt = time.perf_counter() - t0
     assert ref.status == O.OK
     return {"value": n / dt, "unit": "tokens/s", "cores": O.max_threads(), "kind": "oracle",
+            "cpu_model": cpu_model(), "host_cpus": os.cpu_count(),
             "sample": (f"the whole batch" if n == w.n_tokens else f"first {n} tokens of the batch")
                       + f" ({sup.size} supervised rows, full vocabulary {w.vocab}, logits generated "
                         f"before the clock starts), {dt:.1f} s"}
