@@ -21,8 +21,8 @@ bool vpt_allowed(int v) { return v >= 1 && v <= kMaxVpt; }
 // Default cap on packs per thread.  25 packs of both rows fit in 256 VGPRs
 // (two workgroups per CU) and cut a V = 151936 bf16 row into 3 chunks; larger
 // chunks measured faster than more workgroups per CU with smaller chunks
-// (3 chunks: 7.23 ms, 4: 7.47 ms, 6 chunks at three workgroups per CU: 7.42 ms
-// for 65,536 rows, same process).
+// (3 chunks: 6.97 ms, 4: 7.46 ms, 5: 7.39 ms, 6 chunks at three workgroups
+// per CU: 7.40 ms for 65,536 rows, same process).
 constexpr int kDefaultVmax = 25;
 
 long long ceil_div(long long a, long long b) { return (a + b - 1) / b; }
