@@ -269,6 +269,19 @@ int turnkl_profile_row_kernel(hipEvent_t before, hipEvent_t after);
  */
 int turnkl_set_row_tiling(int vectors_per_thread);
 
+/*
+ * Bound on the row kernel's wait for the partials of a row's other chunks,
+ * for the calling host thread: a workgroup gives up after this many polls
+ * that find a partial missing (s_sleep between polls), records
+ * TURNKL_ERR_SYNC_TIMEOUT in the workspace and exits, and so does every
+ * workgroup after it; the later kernels of the call see the error and skip
+ * their work.  0 restores the default (2^22 polls, seconds).  The callers are
+ * tests of that error path: a bound of 1 makes a batch of multi-chunk rows
+ * time out at once while every kernel still exits normally.  Returns
+ * TURNKL_ERR_INVALID_ARG for a negative value.
+ */
+int turnkl_set_spin_limit(int polls);
+
 /* ------------------------------------------------------------------------
  * Top-K variant of the loss: the reverse KL on the teacher's top-K support
  * (App. D: Algorithm 1 computes top-K reverse-KL token losses; the

@@ -47,7 +47,6 @@ namespace {
 constexpr float kLog2e = 1.4426950408889634f;
 constexpr float kLn2 = 0.6931471805599453f;
 constexpr int kRowWaves = kRowThreads / kWave;
-constexpr int kSpinLimit = 1 << 22;
 // Reference magnitude (log2 units, i.e. logits times log2 e) above which a
 // chunk, and then its row, subtracts its references per element.  Below it
 // the fast path's error term, a few u |m_s - m_t|, stays under 1e-5.
@@ -565,7 +564,7 @@ __global__ __launch_bounds__(kRowThreads) void rowkl_kernel(RowParams p) {
         unsigned long long x;
         int spins = 0;
         while (((x = __hip_atomic_load(slot + q, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT)) >> 32) == 0ull) {
-          if (++spins > kSpinLimit) {
+          if (++spins > p.spin_limit) {
             s_timeout = 1;
             break;
           }

@@ -15,6 +15,7 @@ namespace {
 thread_local hipEvent_t t_row_before = nullptr;
 thread_local hipEvent_t t_row_after = nullptr;
 thread_local int t_vpt_override = 0;
+thread_local int t_spin_limit = 0;
 
 bool vpt_allowed(int v) { return v >= 1 && v <= kMaxVpt; }
 
@@ -29,6 +30,7 @@ long long ceil_div(long long a, long long b) { return (a + b - 1) / b; }
 }  // namespace
 
 int thread_tiling_override() { return t_vpt_override; }
+int thread_spin_limit() { return t_spin_limit > 0 ? t_spin_limit : kDefaultSpinLimit; }
 
 // k = ceil(P / (256 * vmax)) chunks of a row of P packs, with boundaries
 // from chunk_start: 1 KiB-aligned when that keeps vpt = ceil(widest / 256)
@@ -268,6 +270,7 @@ int turnkl_fwd_bwd(const void* student_logits, int64_t ld_student, const void* t
   rp.align = tiling.align;
   rp.bf16 = dtype == TURNKL_BF16;
   rp.lse = ex.lse;
+  rp.spin_limit = thread_spin_limit();
   const bool prof = t_row_before && t_row_after;
   if (prof && hipEventRecord(t_row_before, stream) != hipSuccess) return TURNKL_ERR_HIP;
   if (launch_rows(rp, tiling, stream) != hipSuccess) return TURNKL_ERR_HIP;
@@ -441,6 +444,12 @@ const char* turnkl_status_string(int status) {
 int turnkl_profile_row_kernel(hipEvent_t before, hipEvent_t after) {
   t_row_before = before;
   t_row_after = after;
+  return TURNKL_OK;
+}
+
+int turnkl_set_spin_limit(int polls) {
+  if (polls < 0) return TURNKL_ERR_INVALID_ARG;
+  t_spin_limit = polls;
   return TURNKL_OK;
 }
 

@@ -276,8 +276,13 @@ struct RowParams {
   int n_chunks;  // <= kMaxChunks
   int align;     // chunk boundary alignment in packs (chunk_start)
   int bf16;
+  int spin_limit;  // polls of a missing row-mate partial before the call times out
   float* lse;    // [n_rows][2] log-partition functions of both rows, or null
 };
+
+// Default bound on those polls (with s_sleep between them: seconds).
+constexpr int kDefaultSpinLimit = 1 << 22;
+int thread_spin_limit();
 
 hipError_t launch_rows(const RowParams& p, const RowTiling& t, hipStream_t s);
 

@@ -34,7 +34,7 @@ F32 = 1
 # Names of every entry point include/turnkl.h declares.
 EXPORTS = ("turnkl_workspace_bytes", "turnkl_fwd_bwd", "turnkl_get_status",
            "turnkl_get_segments", "turnkl_alpha_schedule", "turnkl_status_string",
-           "turnkl_profile_row_kernel", "turnkl_set_row_tiling",
+           "turnkl_profile_row_kernel", "turnkl_set_row_tiling", "turnkl_set_spin_limit",
            "turnkl_topk_workspace_bytes", "turnkl_fwd_bwd_topk",
            "turnkl_depth_default_config", "turnkl_depth_init", "turnkl_depth_plan",
            "turnkl_depth_update", "turnkl_loss_share", "turnkl_budget_report",
@@ -114,6 +114,8 @@ def lib() -> ctypes.CDLL:
         l.turnkl_profile_row_kernel.argtypes = [c.c_void_p, c.c_void_p]
         l.turnkl_set_row_tiling.restype = c.c_int
         l.turnkl_set_row_tiling.argtypes = [c.c_int]
+        l.turnkl_set_spin_limit.restype = c.c_int
+        l.turnkl_set_spin_limit.argtypes = [c.c_int]
         l.turnkl_topk_workspace_bytes.restype = c.c_size_t
         l.turnkl_topk_workspace_bytes.argtypes = [c.c_int64, c.c_int32, c.c_int32]
         l.turnkl_fwd_bwd_topk.restype = c.c_int
@@ -160,6 +162,13 @@ def set_row_tiling(vectors_per_thread: int) -> None:
     rc = lib().turnkl_set_row_tiling(vectors_per_thread)
     if rc != OK:
         raise TurnKLError(rc, "turnkl_set_row_tiling")
+
+
+def set_spin_limit(polls: int) -> None:
+    """Bound on the row kernel's cross-workgroup wait for this thread (0: default)."""
+    rc = lib().turnkl_set_spin_limit(polls)
+    if rc != OK:
+        raise TurnKLError(rc, "turnkl_set_spin_limit")
 
 
 def profile_row_kernel(before, after) -> None:

@@ -64,6 +64,10 @@ def test_workspace_bytes():
         T.set_row_tiling(26)
     with pytest.raises(T.TurnKLError):
         T.set_row_tiling(-1)
+    with pytest.raises(T.TurnKLError):
+        T.set_spin_limit(-1)
+    T.set_spin_limit(5)
+    T.set_spin_limit(0)
 
 
 def _call(**kw):

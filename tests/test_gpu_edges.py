@@ -428,6 +428,39 @@ def test_large_logit_offsets_keep_full_accuracy(shift_s, shift_t, dtype, gpu):
 # data errors detected on the device
 
 
+def test_exchange_timeout_is_reported_and_the_workspace_recovers(gpu):
+    """A bound of one poll on the row kernel's wait for its row mates (set
+    from the host) makes multi-chunk rows time out: the call reports
+    TURNKL_ERR_SYNC_TIMEOUT, the loss is NaN, every kernel exits, and the next
+    call on the same workspace, with the default bound, is correct."""
+    log("exchange timeout forced from the host")
+    traj, turn, mask, zs_h, zt_h = make_batch(90, n_traj=40, max_turns=6, V=32000,
+                                              dtype="bf16", max_len=24)
+    zs, zt = to_device_logits(zs_h), to_device_logits(zt_h)
+    turn_d, traj_d, mask_d = ids_to_device(traj, turn, mask)
+    T.set_row_tiling(3)  # six chunks per row
+    try:
+        ws = T.Workspace(len(traj), 32000, T.BF16, 8)
+        T.set_spin_limit(1)
+        try:
+            loss, _, _, _, _ = T.fwd_bwd(zs, zt, turn_d, traj_d, mask_d, 0.4, max_turns=8,
+                                         workspace=ws, check=False)
+            torch.cuda.synchronize()
+        finally:
+            T.set_spin_limit(0)
+        assert ws.status() == T.ERR_SYNC_TIMEOUT
+        assert torch.isnan(loss).all()
+        stats = T.new_turn_stats(8)
+        loss, g, _, kl, ws = T.fwd_bwd(zs, zt, turn_d, traj_d, mask_d, 0.4, max_turns=8,
+                                       turn_stats=stats, token_kl=True, workspace=ws)
+        torch.cuda.synchronize()
+    finally:
+        T.set_row_tiling(0)
+    ref = O.fwd_bwd(traj, turn, mask, 0.4, 8, lambda r: (zs_h[r], zt_h[r]), O.DTYPE_BF16, 1.0,
+                    list(range(0, len(traj), 7)))
+    check_all((loss, g, stats, kl, ws), ref, mask, 1.0, list(range(0, len(traj), 7)))
+
+
 @pytest.mark.parametrize("case", ["pad_mask", "turn_high", "turn_negative", "traj_down",
                                   "turn_down", "split_turn", "first_error_wins"])
 def test_device_errors_match_oracle(case, gpu):
