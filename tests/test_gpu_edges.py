@@ -414,7 +414,8 @@ def test_rows_mixing_fast_and_offset_chunks(dtype, vpt, gpu):
 
 
 @pytest.mark.parametrize("shift_s,shift_t,dtype", [(5000.0, 5000.0, "f32"), (-3000.0, 3000.0, "f32"),
-                                                   (1000.0, 1000.0, "bf16"), (-96.0, 0.0, "bf16")])
+                                                   (1000.0, 1000.0, "bf16"), (-96.0, 0.0, "bf16"),
+                                                   (1e6, -1e6, "f32"), (1e30, -1e30, "f32")])
 def test_large_logit_offsets_keep_full_accuracy(shift_s, shift_t, dtype, gpu):
     """KL and its gradient do not depend on a constant added to a row of
     either model; computed against the chunk references they keep the same
