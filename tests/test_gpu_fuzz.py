@@ -16,7 +16,7 @@ from test_gpu_edges import make_batch
 
 pytestmark = pytest.mark.gpu
 
-N_CASES = 64
+N_CASES = 128
 
 
 def _case(k):
@@ -103,7 +103,7 @@ def test_random_configuration(k, gpu):
     check_grad_rows(g, ref, c["grad_scale"], rows, mask)
 
 
-N_TOPK_CASES = 24
+N_TOPK_CASES = 48
 
 
 @pytest.mark.parametrize("k", range(N_TOPK_CASES))
