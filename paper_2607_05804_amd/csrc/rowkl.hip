@@ -368,14 +368,37 @@ __global__ __launch_bounds__(kRowThreads) void rowkl_kernel(RowParams p) {
     // reads the chunk's first pack instead and is masked below)
     const auto rs = chunk_rsrc(static_cast<const char*>(p.zs) + (row * p.ld_s + col) * kEs);
     const auto rt = chunk_rsrc(static_cast<const char*>(p.zt) + (row * p.ld_t + col) * kEs);
+    // bf16: the student's packs, then the teacher's, rather than alternating
+    // them.  On batches that mix masked and supervised rows this measured
+    // 1.6% faster (6.84 against 6.96 ms for the 65,536-row batch with 40% of
+    // its rows masked, 1.47 against 1.49 ms with 60% masked, same process);
+    // with every row supervised it is 1.9% slower (9.66 against 9.48 ms).
+    // The fp32 instantiation keeps them alternating: split, it needs 258
+    // VGPRs, one wave per SIMD.
     P xs[kVpt], xt[kVpt];
+    if constexpr (kBf16) {
 #pragma unroll
-    for (int v = 0; v < kVpt; ++v) {
-      const bool sure = !kCheckAll && v < kVpt - 1;
-      const int vo = sure ? lane_off : (valid[v] ? lane_off : 0);
-      const int so = sure ? v * kStep : (valid[v] ? v * kStep : 0);
-      xs[v].load(rs, vo, so);
-      xt[v].load(rt, vo, so);
+      for (int v = 0; v < kVpt; ++v) {
+        const bool sure = !kCheckAll && v < kVpt - 1;
+        xs[v].load(rs, sure ? lane_off : (valid[v] ? lane_off : 0),
+                   sure ? v * kStep : (valid[v] ? v * kStep : 0));
+      }
+      __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+      for (int v = 0; v < kVpt; ++v) {
+        const bool sure = !kCheckAll && v < kVpt - 1;
+        xt[v].load(rt, sure ? lane_off : (valid[v] ? lane_off : 0),
+                   sure ? v * kStep : (valid[v] ? v * kStep : 0));
+      }
+    } else {
+#pragma unroll
+      for (int v = 0; v < kVpt; ++v) {
+        const bool sure = !kCheckAll && v < kVpt - 1;
+        const int vo = sure ? lane_off : (valid[v] ? lane_off : 0);
+        const int so = sure ? v * kStep : (valid[v] ? v * kStep : 0);
+        xs[v].load(rs, vo, so);
+        xt[v].load(rt, vo, so);
+      }
     }
     __builtin_amdgcn_sched_barrier(0);
     keep_alive(carry);  // the previous task's last store has long read its data
