@@ -269,7 +269,7 @@ __device__ inline void merge_chunk(bool offset, const float* w, float rs, float 
 // packs long, so every pack v < kVpt - 1 lies inside the chunk and only the
 // last one is predicated (kCheckAll: all of them, for the unaligned scalar
 // path, whose chunks carry no such guarantee).
-template <bool kBf16, int kEpv, int kVpt, bool kCheckAll>
+template <bool kBf16, int kEpv, int kVpt, bool kCheckAll, bool kSplit>
 __global__ __launch_bounds__(kRowThreads) void rowkl_kernel(RowParams p) {
   using P = Pack<kBf16, kEpv>;
   constexpr int kEs = kBf16 ? 2 : 4;
@@ -286,6 +286,12 @@ __global__ __launch_bounds__(kRowThreads) void rowkl_kernel(RowParams p) {
   __shared__ int s_timeout;
 
   if (p.hdr->err_key != kNoError) return;
+  // Two launches, one per load order (see the loads below): the split order
+  // runs when at most 90% of the rows are supervised, the other one exits
+  // here before taking any work.
+  if (p.pick_order &&
+      (10ll * __builtin_amdgcn_readfirstlane(p.hdr->n_sup) < 9ll * (long long)p.n_rows) != kSplit)
+    return;
   const int tid = threadIdx.x;
   const int lane = tid & (kWave - 1);
   const int wid = tid / kWave;
@@ -368,15 +374,18 @@ __global__ __launch_bounds__(kRowThreads) void rowkl_kernel(RowParams p) {
     // reads the chunk's first pack instead and is masked below)
     const auto rs = chunk_rsrc(static_cast<const char*>(p.zs) + (row * p.ld_s + col) * kEs);
     const auto rt = chunk_rsrc(static_cast<const char*>(p.zt) + (row * p.ld_t + col) * kEs);
-    // bf16: the student's packs, then the teacher's, rather than alternating
-    // them.  On batches that mix masked and supervised rows this measured
-    // 1.6% faster (6.84 against 6.96 ms for the 65,536-row batch with 40% of
-    // its rows masked, 1.47 against 1.49 ms with 60% masked, same process);
-    // with every row supervised it is 1.9% slower (9.66 against 9.48 ms).
-    // The fp32 instantiation keeps them alternating: split, it needs 258
-    // VGPRs, one wave per SIMD.
+    // Load order.  kSplit: the student's packs, then the teacher's; else
+    // alternating.  On batches that mix masked and supervised rows the split
+    // order measured 1.6% faster (6.84 against 6.96 ms for the 65,536-row
+    // batch with 40% of its rows masked, 1.47 against 1.49 ms with 60%
+    // masked, same process); with every row supervised it is 1.9% slower
+    // (9.66 against 9.48 ms), so the host launches both orders and each
+    // call runs one (see rowkl_kernel's first lines).  The two orders are
+    // separate kernels: in one kernel the bf16 instantiation needs 258 VGPRs
+    // (one wave per SIMD), and so does the fp32 one with the split order,
+    // which therefore always alternates.
     P xs[kVpt], xt[kVpt];
-    if constexpr (kBf16) {
+    if constexpr (kSplit) {
 #pragma unroll
       for (int v = 0; v < kVpt; ++v) {
         const bool sure = !kCheckAll && v < kVpt - 1;
@@ -739,11 +748,11 @@ int cu_count() {
   return n;
 }
 
-template <bool kBf16, int kEpv, int kVpt, bool kCheckAll>
+template <bool kBf16, int kEpv, int kVpt, bool kCheckAll, bool kSplit = false>
 hipError_t launch_one(const RowParams& p, hipStream_t s) {
   static const int occ = [] {
     int n = 0;
-    if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&n, rowkl_kernel<kBf16, kEpv, kVpt, kCheckAll>,
+    if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&n, rowkl_kernel<kBf16, kEpv, kVpt, kCheckAll, kSplit>,
                                                      kRowThreads, 0) != hipSuccess || n < 1)
       n = 1;
     return n;
@@ -752,15 +761,29 @@ hipError_t launch_one(const RowParams& p, hipStream_t s) {
   long long grid = (long long)occ * cu_count();
   if (grid > tasks) grid = tasks;
   if (grid < 1) return hipSuccess;
-  rowkl_kernel<kBf16, kEpv, kVpt, kCheckAll><<<dim3((unsigned)grid), dim3(kRowThreads), 0, s>>>(p);
+  rowkl_kernel<kBf16, kEpv, kVpt, kCheckAll, kSplit><<<dim3((unsigned)grid), dim3(kRowThreads), 0, s>>>(p);
   return hipGetLastError();
+}
+
+// bf16: both load orders, each kernel checking which one the call uses;
+// fp32: the alternating order alone.
+template <bool kBf16, int kEpv, int kVpt>
+hipError_t launch_orders(const RowParams& p, hipStream_t s) {
+  if constexpr (kBf16) {
+    RowParams q = p;
+    q.pick_order = 1;
+    if (hipError_t e = launch_one<kBf16, kEpv, kVpt, false, true>(q, s); e != hipSuccess) return e;
+    return launch_one<kBf16, kEpv, kVpt, false, false>(q, s);
+  } else {
+    return launch_one<kBf16, kEpv, kVpt, false, false>(p, s);
+  }
 }
 
 template <bool kBf16, int kEpv>
 hipError_t launch_vpt(const RowParams& p, int vpt, hipStream_t s) {
   switch (vpt) {
 #define TURNKL_CASE(n) \
-    case n: return launch_one<kBf16, kEpv, n, false>(p, s);
+    case n: return launch_orders<kBf16, kEpv, n>(p, s);
     TURNKL_CASE(1) TURNKL_CASE(2) TURNKL_CASE(3) TURNKL_CASE(4) TURNKL_CASE(5) TURNKL_CASE(6)
     TURNKL_CASE(7) TURNKL_CASE(8) TURNKL_CASE(9) TURNKL_CASE(10) TURNKL_CASE(11) TURNKL_CASE(12)
     TURNKL_CASE(13) TURNKL_CASE(14) TURNKL_CASE(15) TURNKL_CASE(16) TURNKL_CASE(17) TURNKL_CASE(18)

@@ -16,8 +16,9 @@
 //               trajectory / end, supervised counts (integer atomics).
 //   seg_link    per segment: ordering check against the previous segment,
 //               outcome-flag check against the trajectory's first segment,
-//               segment length, trajectory head segment, T_b, N_b and B, and
-//               the survivors n_t of the turn-support floor.
+//               segment length, trajectory head segment, T_b, N_b and B, the
+//               batch's supervised-token count, and the survivors n_t of the
+//               turn-support floor.
 //   seg_valid   (turn-support floor only) per segment: T_vb, the valid
 //               supervised turns of each trajectory (n_t >= n_min).
 //   token_weights per token: w_i and grad_scale * w_i, clears this call's
@@ -124,6 +125,7 @@ __global__ __launch_bounds__(kScanThreads) void seg_offsets(Ws ws, long long nbl
     h->ticket = 0u;
     h->n_seg = carry;
     h->b_eff = 0;
+    h->n_sup = 0;
     drain_stores();
   }
 }
@@ -189,6 +191,7 @@ __global__ __launch_bounds__(kSegThreads) void seg_link(SegParams p, Ws ws) {
     if (n > 0) {
       atomicAdd(&ws.traj_T[head], 1);
       if (atomicAdd(&ws.traj_N[head], n) == 0) atomicAdd(&ws.hdr->b_eff, 1);
+      atomicAdd(&ws.hdr->n_sup, n);
       if (p.floor_on && t >= 0 && t < p.max_turns) atomicAdd(&ws.turn_surv[t], 1);
     }
   }

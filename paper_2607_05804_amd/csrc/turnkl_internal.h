@@ -48,7 +48,8 @@ struct Header {
   unsigned int ticket;         // row-kernel work counter
   int n_seg;                   // number of segments
   int b_eff;                   // trajectories with >= 1 supervised token
-  int pad[59];
+  int n_sup;                   // supervised tokens
+  int pad[58];
 };
 static_assert(sizeof(Header) == 256, "header is one 256-byte line");
 
@@ -277,6 +278,8 @@ struct RowParams {
   int align;     // chunk boundary alignment in packs (chunk_start)
   int bf16;
   int spin_limit;  // polls of a missing row-mate partial before the call times out
+  int pick_order;  // 1: one of two launches (one per load order) that picks by
+                   // the supervised share of the rows; 0: the only launch
   float* lse;    // [n_rows][2] log-partition functions of both rows, or null
 };
 

@@ -125,6 +125,22 @@ def test_full_vocabulary_default_tiling(dtype, gpu):
     check_all(out, ref, mask, 1.0, rows)
 
 
+@pytest.mark.parametrize("share", [1.0, 0.9, 0.89, 0.5])
+def test_both_load_orders(share, gpu):
+    """The bf16 row kernel runs in one of two load orders, chosen on the device
+    from the supervised share of the rows (alternating above 90%, split
+    otherwise); both give the oracle's results at the default tiling."""
+    log(f"load order, supervised share {share}")
+    traj, turn, mask, zs, zt = make_batch(95, n_traj=4, max_turns=5, V=151936, dtype="bf16",
+                                          pad=False, min_len=5, max_len=10)
+    n = len(traj)
+    k = int(round(share * n))
+    mask = np.zeros(n, np.uint8)
+    mask[np.random.default_rng(3).permutation(n)[:k]] = 1
+    out, ref, rows = run_both(traj, turn, mask, zs, zt)
+    check_all(out, ref, mask, 1.0, rows)
+
+
 @pytest.mark.parametrize("V,dtype", [(6553600, "bf16"), (3276800, "f32"), (1048575, "bf16")])
 def test_vocabularies_at_the_chunk_limit(V, dtype, gpu):
     """The widest rows the host accepts: 128 chunks per row, on the vector path
