@@ -230,3 +230,38 @@ def test_topk_workspace_bytes():
 ])
 def test_topk_host_rejects_bad_arguments_before_launch(kw, code):
     assert _call_topk(**kw) == code
+
+
+def test_header_is_plain_c_and_links(tmp_path):
+    """include/turnkl.h compiles as C11 with warnings as errors, and a C
+    program linked against the library calls its host entry points (no GPU
+    is touched)."""
+    import shutil
+    import subprocess
+    gcc = shutil.which("gcc")
+    if gcc is None:
+        pytest.skip("no C compiler")
+    src = tmp_path / "abi.c"
+    src.write_text(r'''
+#include <stdio.h>
+#include "turnkl.h"
+int main(void) {
+  size_t b = turnkl_workspace_bytes(1000, 151936, TURNKL_BF16, 50);
+  turnkl_depth_config c;
+  turnkl_depth_default_config(&c);
+  if (b == 0 || c.h_max < c.h_min) return 1;
+  if (turnkl_alpha_schedule(5, 10, 0.0, 1.0) != 0.5) return 2;
+  printf("%s\n", turnkl_status_string(TURNKL_ERR_SYNC_TIMEOUT));
+  return 0;
+}
+''')
+    exe = tmp_path / "abi"
+    libdir = os.path.dirname(T.LIB_PATH)
+    cmd = [gcc, "-std=c11", "-Wall", "-Werror", "-D__HIP_PLATFORM_AMD__",
+           "-I", os.path.join(ROOT, "include"), "-I", "/opt/rocm/include", str(src),
+           "-L", libdir, "-lturnkl", f"-Wl,-rpath,{libdir}", "-o", str(exe)]
+    r = subprocess.run(cmd, capture_output=True, text=True)
+    assert r.returncode == 0, r.stderr
+    r = subprocess.run([str(exe)], capture_output=True, text=True, timeout=60)
+    assert r.returncode == 0, (r.returncode, r.stderr)
+    assert r.stdout.strip() == T.status_string(T.ERR_SYNC_TIMEOUT)
