@@ -100,6 +100,33 @@ def test_peaked_full_size_alpha_sweep(gpu):
     _full_size("peaked", gpu)
 
 
+def test_peaked_full_size_every_row_supervised(gpu):
+    """The peaked batch (16,534 rows x V = 151,936) with every row supervised:
+    the row kernel's alternating load order, chosen on the device when more
+    than 90% of the rows are supervised, at full width against the oracle."""
+    w = synth.make("peaked")
+    mask_h = np.ones(w.n_tokens, np.uint8)
+    log(f"parity peaked, every row supervised: N={w.n_tokens} V={w.vocab}")
+    zs, zt = w.device_logits()
+    rows = sample_rows(mask_h, 24, 0, seed=2)
+    ref = O.fwd_bwd(w.traj_id, w.turn_id, mask_h, w.alphas[0], w.max_turns,
+                    device_row_source(zs, zt), oracle_dtype(zs.dtype), 1.0, rows)
+    assert ref.status == O.OK
+    turn, traj, mask = ids_to_device(w.traj_id, w.turn_id, mask_h)
+    stats = T.new_turn_stats(w.max_turns)
+    loss, g, _, kl, ws = T.fwd_bwd(zs, zt, turn, traj, mask, w.alphas[0], max_turns=w.max_turns,
+                                   turn_stats=stats, token_kl=True)
+    torch.cuda.synchronize()
+    check_segments(ws, ref.seg)
+    check_loss(loss, ref.loss)
+    check_token_kl(kl, ref.kl, mask_h)
+    check_stats(stats, ref.stats)
+    worst = check_grad_rows(g, ref, 1.0, rows, mask_h)
+    log(f"  loss gpu={loss.tolist()} ref={ref.loss} worst grad err={worst:.2e}")
+    del g, zs, zt
+    torch.cuda.empty_cache()
+
+
 def test_long_horizon_full_size(gpu):
     _full_size("long_horizon", gpu)
 
