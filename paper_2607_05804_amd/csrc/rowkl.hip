@@ -12,15 +12,21 @@
 //   M_t = max(b) log2(e),  S_t = sum 2^(b log2(e) - M_t).
 //
 // Work decomposition.  A row of V elements (V / epv packs of 16 bytes) is cut
-// into n_chunks balanced chunks (pack counts differ by at most one); each of
-// a workgroup's 256 threads holds up to vpt packs.  One workgroup owns one
-// (row, chunk) task: it loads its chunk of both rows into registers, reduces
-// the chunk's partials, publishes them as seven tagged 64-bit words (see the
-// row merge below), reads its row mates' words, merges all chunks in chunk
-// order (so every workgroup of the row computes bit-identical row scalars),
-// and writes its chunk of the gradient straight from registers.  Every logit is read from HBM exactly
-// once and every gradient element written once: 3 V s bytes per supervised
-// row, V s per unsupervised row (zeros only).
+// into n_chunks chunks whose boundaries chunk_start places on 1 KiB (or
+// 128-byte) multiples from the row start when the host's tiling allows, else
+// balanced; each of a workgroup's 256 threads holds up to vpt packs.  One
+// workgroup owns one (row, chunk) task: it loads its chunk of both rows into
+// registers, reduces the chunk's partials, publishes them as seven tagged
+// 64-bit words (see the row merge below), reads its row mates' words, merges
+// all chunks in chunk order (so every workgroup of the row computes
+// bit-identical row scalars), and writes its chunk of the gradient straight
+// from registers.  Every logit is read from HBM exactly once and every
+// gradient element written once: 3 V s bytes per supervised row, V s per
+// unsupervised row (zeros only).
+//
+// Scheduling.  A wave's priority rises with its task's progress (loads,
+// partial sums, stores), and the bf16 kernel comes in two load orders, one
+// of which each call runs (both explained where they are set).
 //
 // Tasks are handed out by an atomic ticket in row-major order, so a
 // workgroup only ever waits for tasks that running workgroups already hold
