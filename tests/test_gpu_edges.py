@@ -445,6 +445,56 @@ def test_large_logit_offsets_keep_full_accuracy(shift_s, shift_t, dtype, gpu):
 # data errors detected on the device
 
 
+def test_concurrent_calls_on_two_streams(gpu):
+    """Two calls with distinct workspaces, enqueued on two streams at once,
+    give bit for bit what the same calls give one after the other (the row
+    kernels' exchanges and tickets are per workspace)."""
+    log("two concurrent calls")
+    batches = []
+    for seed in (70, 71):
+        traj, turn, mask, zs_h, zt_h = make_batch(seed, n_traj=60, max_turns=6, V=32000,
+                                                  dtype="bf16", max_len=30)
+        zs, zt = to_device_logits(zs_h), to_device_logits(zt_h)
+        ids = ids_to_device(traj, turn, mask)
+        batches.append((zs, zt) + ids + (len(traj),))
+
+    def run(b, grad, stats, kl, ws):
+        zs, zt, turn_d, traj_d, mask_d, n = b
+        loss, _, _, _, _ = T.fwd_bwd(zs, zt, turn_d, traj_d, mask_d, 0.4, grad=grad, max_turns=8,
+                                     turn_stats=stats, token_kl=kl, workspace=ws, check=False)
+        return loss
+
+    T.set_row_tiling(3)  # six chunks per row
+    try:
+        outs = []
+        for mode in ("sequential", "concurrent"):
+            bufs = [(torch.empty_like(b[0]), T.new_turn_stats(8),
+                     torch.empty(b[5], dtype=torch.float32, device="cuda"),
+                     T.Workspace(b[5], 32000, T.BF16, 8)) for b in batches]
+            torch.cuda.synchronize()
+            if mode == "sequential":
+                losses = [run(b, *bf) for b, bf in zip(batches, bufs)]
+            else:
+                streams = [torch.cuda.Stream(), torch.cuda.Stream()]
+                losses = []
+                for st, b, bf in zip(streams, batches, bufs):
+                    st.wait_stream(torch.cuda.current_stream())
+                    with torch.cuda.stream(st):
+                        losses.append(run(b, *bf))
+                for st in streams:
+                    torch.cuda.current_stream().wait_stream(st)
+            torch.cuda.synchronize()
+            for bf in bufs:
+                assert bf[3].status() == T.OK
+            outs.append([(l.cpu(), bf[0].view(torch.int16).cpu(), bf[1].cpu(), bf[2].cpu())
+                         for l, bf in zip(losses, bufs)])
+    finally:
+        T.set_row_tiling(0)
+    for a, b in zip(outs[0], outs[1]):
+        for x, y in zip(a, b):
+            assert torch.equal(x, y)
+
+
 def test_exchange_timeout_is_reported_and_the_workspace_recovers(gpu):
     """A bound of one poll on the row kernel's wait for its row mates (set
     from the host) makes multi-chunk rows time out: the call reports
