@@ -106,3 +106,53 @@ def test_topk_graph_replays_equal_eager(gpu):
         assert torch.equal(grad.view(torch.int16), ref[1].view(torch.int16)), r
         assert torch.equal(gk, ref[2]) and torch.equal(stats, ref[3]), r
     log(f"top-K graph replays ok: loss={loss_g.tolist()}")
+
+
+def test_graph_replays_follow_the_mask(gpu):
+    """The bf16 row kernel's load order is chosen on the device from the
+    supervised share of the rows, so one captured call replayed with a mixed
+    mask and with every row supervised (written into the same mask buffer
+    between replays) equals the eager call for each mask, bit for bit."""
+    w = synth.make("agent")
+    zs_h, zt_h = w.host_logits(0, w.n_tokens)
+    zs, zt = to_device_logits(zs_h), to_device_logits(zt_h)
+    turn, traj, mask = ids_to_device(w.traj_id, w.turn_id, w.loss_mask)
+    masks = [mask.clone(), (traj >= 0).to(torch.uint8)]
+    assert masks[0].float().mean().item() < 0.9 and masks[1].float().mean().item() > 0.9
+    n, V = zs.shape
+    ws = T.Workspace(n, V, T.BF16, w.max_turns)
+    grad = torch.empty_like(zs)
+    kl = torch.empty(n, dtype=torch.float32, device=gpu)
+    stats = T.new_turn_stats(w.max_turns)
+    s = torch.cuda.Stream()
+    s.wait_stream(torch.cuda.current_stream())
+    refs = []
+    with torch.cuda.stream(s):
+        for m in masks:
+            mask.copy_(m)
+            loss, *_ = T.fwd_bwd(zs, zt, turn, traj, mask, 0.3, grad=grad, max_turns=w.max_turns,
+                                 turn_stats=stats, token_kl=kl, workspace=ws, check=False)
+            s.synchronize()
+            assert ws.status() == T.OK
+            refs.append((loss.clone(), grad.clone(), kl.clone(), stats.clone()))
+        mask.copy_(masks[0])
+        g = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(g, stream=s):
+            loss_g, *_ = T.fwd_bwd(zs, zt, turn, traj, mask, 0.3, grad=grad,
+                                   max_turns=w.max_turns, turn_stats=stats, token_kl=kl,
+                                   workspace=ws, check=False)
+    torch.cuda.current_stream().wait_stream(s)
+    for r in range(6):
+        k = r % 2
+        mask.copy_(masks[k])  # eager work between replays
+        grad.fill_(7)
+        kl.zero_()
+        stats.fill_(5)
+        g.replay()
+        torch.cuda.synchronize()
+        assert ws.status() == T.OK
+        ref = refs[k]
+        assert torch.equal(loss_g, ref[0]), r
+        assert torch.equal(grad.view(torch.int16), ref[1].view(torch.int16)), r
+        assert torch.equal(kl, ref[2]) and torch.equal(stats, ref[3]), r
+    log(f"graph replays follow the mask: losses {[x[0].tolist() for x in refs]}")
