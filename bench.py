@@ -42,6 +42,10 @@ def row_kernel_digest() -> str:
     return h.hexdigest()[:16]
 
 
+WORKLOAD_NAMES = {"long_horizon": "long-horizon agent batch", "peaked": "peaked-teacher batch",
+                  "stress": "stress batch"}
+
+
 def committed_traffic():
     """HBM bytes per row-kernel launch from the committed counter summary,
     or None when it is missing or was taken on a different kernel source."""
@@ -392,6 +396,9 @@ def main() -> int:
     ap.add_argument("--copy-probe", type=float, default=0.0, metavar="GIB",
                     help="instead of the step, time a plain device copy of this many GiB "
                          "(bandwidth context and counter calibration)")
+    ap.add_argument("--workload", default="long_horizon", choices=sorted(WORKLOAD_NAMES),
+                    help="the batch to time (the default is the headline batch; the others "
+                         "are the full-size parity batches, 16,534 and 131,072 tokens)")
     ap.add_argument("--sustain", type=float, default=0.0, metavar="SECONDS",
                     help="instead of the measurements, run the timed call back to back for "
                          "this long and report its rate (for clock and power readings under "
@@ -413,7 +420,7 @@ def main() -> int:
 
     T.lib()  # fails loudly when the HIP library is missing
     dev = torch.device("cuda:0")
-    w = synth.make("long_horizon")
+    w = synth.make(args.workload)
     alpha = w.alphas[0]
     n, V = w.n_tokens, w.vocab
     n_sup = w.n_supervised
@@ -460,7 +467,8 @@ def main() -> int:
     es = 2
     row_bytes = n_sup * 3 * V * es + (n - n_sup) * V * es
     achieved = row_bytes / (row_ms * 1e-3) / 1e9
-    traffic = committed_traffic()
+    # the committed counters are those of the headline batch
+    traffic = committed_traffic() if args.workload == "long_horizon" else None
     out = {
         "metric": "fused turn-KL fwd+bwd tokens/sec and achieved HBM GB/s (% of peak), V=151936",
         "value": n * args.steps / elapsed,
@@ -475,9 +483,9 @@ def main() -> int:
         "dtype": "f32",
         "data": "synthetic",
         "config": {
-            "workload": f"long-horizon agent batch: {n} tokens x V={V} bf16 logits, "
-                        f"{int(w.traj_id.max()) + 1} trajectories, 40% observation-masked, "
-                        f"alpha={alpha}",
+            "workload": f"{WORKLOAD_NAMES[args.workload]}: {n} tokens x V={V} bf16 logits, "
+                        f"{int(w.traj_id.max()) + 1} trajectories, "
+                        f"{round(100 * (1 - n_sup / n))}% of tokens masked, alpha={alpha}",
             "n_tokens": n, "vocab": V, "supervised_tokens": n_sup, "logits": "bf16",
             "gradient": "bf16, out of place", "parallelism": "single GPU",
         },
