@@ -179,8 +179,12 @@ def profile_row_kernel(before, after) -> None:
 
 
 def _options(n: int, support_floor: int, support_frac: float, success, outcome_stats,
-             token_weights=None, token_lse=None):
+             token_weights=None, token_lse=None, device=None):
     """turnkl_options for the keyword arguments, or None when all are off."""
+    for t, name in ((success, "success"), (token_weights, "token_weights"),
+                    (token_lse, "token_lse")):
+        if t is not None and device is not None and t.device != device:
+            raise ValueError(f"{name} must be on {device}, not {t.device}")
     if (not support_floor and not support_frac and success is None and outcome_stats is None
             and token_weights is None and token_lse is None):
         return None
@@ -210,6 +214,36 @@ def _row_stride(t: torch.Tensor) -> int:
 
 def _ptr(t: torch.Tensor | None):
     return None if t is None else ctypes.c_void_p(t.data_ptr())
+
+
+def _need(t: torch.Tensor | None, nbytes: int, name: str, device, dtype=None) -> None:
+    """A caller buffer the kernels write or read by size: on the logits'
+    device, contiguous, of the given dtype and at least nbytes long (the C ABI
+    takes bare pointers and cannot check this)."""
+    if t is None:
+        return
+    if t.device != device:
+        raise ValueError(f"{name} must be on {device}, not {t.device}")
+    if dtype is not None and t.dtype != dtype:
+        raise TypeError(f"{name} must be {dtype}, not {t.dtype}")
+    if not t.is_contiguous():
+        raise ValueError(f"{name} must be contiguous")
+    if t.numel() * t.element_size() < nbytes:
+        raise ValueError(f"{name} holds {t.numel() * t.element_size()} bytes; the call needs {nbytes}")
+
+
+def _check_common(student, n, max_turns, turn_id, traj_id, loss_mask, turn_stats, outcome_stats,
+                  kl_t, grad_t):
+    dev = student.device
+    for t, name in ((turn_id, "turn_id"), (traj_id, "traj_id"), (loss_mask, "loss_mask")):
+        _need(t, 0, name, dev)
+    stat_bytes = int(max_turns) * STAT_DTYPE.itemsize
+    _need(turn_stats, stat_bytes, "turn_stats", dev)
+    _need(outcome_stats, 2 * stat_bytes, "outcome_stats", dev)
+    _need(kl_t, 4 * n, "token_kl", dev, torch.float32)
+    if grad_t is not None and grad_t is not student:
+        if grad_t.device != dev or grad_t.dtype != student.dtype or grad_t.shape != student.shape:
+            raise ValueError("grad must match the student logits' device, dtype and shape")
 
 
 class Workspace:
@@ -268,6 +302,8 @@ def fwd_bwd(student: torch.Tensor, teacher: torch.Tensor, turn_id: torch.Tensor,
     dt = _dtype_code(student)
     if teacher.dtype != student.dtype:
         raise TypeError("student and teacher logits must share a dtype")
+    if teacher.shape != student.shape or teacher.device != student.device:
+        raise ValueError("student and teacher logits must share a shape and a device")
     n, v = (int(student.shape[0]), int(student.shape[1])) if student.dim() == 2 else (0, 0)
     for t in (turn_id, traj_id):
         if t.dtype != torch.int32 or t.numel() != n:
@@ -291,6 +327,8 @@ def fwd_bwd(student: torch.Tensor, teacher: torch.Tensor, turn_id: torch.Tensor,
         kl_t = token_kl
     else:
         kl_t = torch.empty(max(n, 1), dtype=torch.float32, device=dev) if token_kl else None
+    _check_common(student, n, max_turns, turn_id, traj_id, loss_mask, turn_stats, outcome_stats,
+                  kl_t, grad_t)
     stream = torch.cuda.current_stream(dev).cuda_stream
     rc = lib().turnkl_fwd_bwd(
         _ptr(student), _row_stride(student) if n else v, _ptr(teacher),
@@ -298,7 +336,8 @@ def fwd_bwd(student: torch.Tensor, teacher: torch.Tensor, turn_id: torch.Tensor,
         float(alpha), float(grad_scale), _ptr(loss), _ptr(grad_t),
         (_row_stride(grad_t) if n else v) if grad_t is not None else 0, _ptr(turn_stats),
         int(max_turns), int(bool(accumulate_stats)), _ptr(kl_t),
-        _options(n, support_floor, support_frac, success, outcome_stats, token_weights, token_lse),
+        _options(n, support_floor, support_frac, success, outcome_stats, token_weights, token_lse,
+                 dev),
         _ptr(workspace.tensor),
         workspace.nbytes, ctypes.c_void_p(stream))
     if rc != OK:
@@ -377,6 +416,14 @@ def fwd_bwd_topk(student: torch.Tensor, teacher_ids: torch.Tensor, teacher_vals:
         kl_t = token_kl
     else:
         kl_t = torch.empty(max(n, 1), dtype=torch.float32, device=dev) if token_kl else None
+    _check_common(student, n, max_turns, turn_id, traj_id, loss_mask, turn_stats, outcome_stats,
+                  kl_t, grad_t)
+    for t, name in ((teacher_ids, "teacher_ids"), (teacher_vals, "teacher_vals")):
+        if t.device != dev or (n and t.stride(1) != 1):
+            raise ValueError(f"{name} must be on the logits' device with unit column stride")
+    if gk is not None and (gk.device != dev or gk.dtype != torch.float32 or gk.dim() != 2
+                           or gk.shape[0] < n or gk.shape[1] != k or (n and gk.stride(1) != 1)):
+        raise ValueError("grad_topk must be float32 [n_tokens, K] with unit column stride")
     stream = torch.cuda.current_stream(dev).cuda_stream
     ld_k = int(teacher_ids.stride(0)) if n else k
     rc = lib().turnkl_fwd_bwd_topk(
@@ -386,7 +433,8 @@ def fwd_bwd_topk(student: torch.Tensor, teacher_ids: torch.Tensor, teacher_vals:
         (_row_stride(grad_t) if n else v) if grad_t is not None else 0, _ptr(gk),
         (int(gk.stride(0)) if n else k) if gk is not None else 0, _ptr(turn_stats),
         int(max_turns), int(bool(accumulate_stats)), _ptr(kl_t),
-        _options(n, support_floor, support_frac, success, outcome_stats, token_weights, token_lse),
+        _options(n, support_floor, support_frac, success, outcome_stats, token_weights, token_lse,
+                 dev),
         _ptr(workspace.tensor),
         workspace.nbytes, ctypes.c_void_p(stream))
     if rc != OK:

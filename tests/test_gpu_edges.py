@@ -571,3 +571,38 @@ def test_device_errors_match_oracle(case, gpu):
                                   check=False)
     assert ws.status() == ref.status
     assert torch.isnan(loss).all()
+
+
+def test_binding_rejects_undersized_or_mismatched_buffers(gpu):
+    """The Python binding checks the size, dtype, shape and device of every
+    caller buffer before calling the C ABI, which takes bare pointers."""
+    traj, turn, mask, zs_h, zt_h = make_batch(97, n_traj=2, V=1024, dtype="bf16")
+    n = len(traj)
+    zs, zt = to_device_logits(zs_h), to_device_logits(zt_h)
+    turn_d, traj_d, mask_d = ids_to_device(traj, turn, mask)
+    call = lambda **kw: T.fwd_bwd(zs, zt, turn_d, traj_d, mask_d, 0.5, max_turns=8, **kw)
+    bad = [
+        dict(turn_stats=T.new_turn_stats(7)),
+        dict(success=torch.zeros(n, dtype=torch.uint8, device="cuda"),
+             outcome_stats=T.new_turn_stats(15)),
+        dict(token_kl=torch.empty(n - 1, dtype=torch.float32, device="cuda")),
+        dict(token_kl=torch.empty(n, dtype=torch.float16, device="cuda")),
+        dict(grad=torch.empty((n, 1000), dtype=torch.bfloat16, device="cuda")),
+        dict(grad=torch.empty((n, 1024), dtype=torch.float32, device="cuda")),
+        dict(token_lse=torch.empty((n, 2), dtype=torch.float32)),
+        dict(token_weights=torch.empty(n - 1, dtype=torch.float32, device="cuda")),
+    ]
+    for kw in bad:
+        with pytest.raises((ValueError, TypeError)):
+            call(**kw)
+    with pytest.raises(ValueError):
+        T.fwd_bwd(zs, zt[:-1], turn_d, traj_d, mask_d, 0.5, max_turns=8)
+    ids = torch.zeros((n, 4), dtype=torch.int32, device="cuda")
+    vals = torch.zeros((n, 4), dtype=torch.float32, device="cuda")
+    with pytest.raises(ValueError):
+        T.fwd_bwd_topk(zs, ids, vals, turn_d, traj_d, mask_d, 0.5, max_turns=8,
+                       grad_topk=torch.empty((n, 3), dtype=torch.float32, device="cuda"))
+    # the same call with correct buffers still works
+    loss, *_ = call(turn_stats=T.new_turn_stats(8), token_kl=True)
+    torch.cuda.synchronize()
+    assert torch.isfinite(loss).all()
