@@ -29,6 +29,7 @@
  *   - Pointers are DEVICE pointers owned by the caller unless marked "host".
  *     The library allocates no memory and keeps no per-call state; all
  *     scratch lives in the caller's workspace.
+ *   - Measurement and test hooks are declared in turnkl_testing.h.
  *   - Work is enqueued on `stream` and is asynchronous; the success path never
  *     synchronises with the host.  Calls on distinct workspaces may run
  *     concurrently; calls sharing a workspace must be stream-ordered.
@@ -142,11 +143,25 @@ typedef struct {
 
 /*
  * Bytes of device workspace turnkl_fwd_bwd needs for this problem (host
- * function, no device access).  Returns 0 when the arguments are invalid
- * (n_tokens < 0, vocab < 1, unknown dtype, max_turns < 1).  The workspace
- * needs no initialisation; it must be 256-byte aligned.
+ * function, no device access; a pure function of its arguments).
+ *
+ * aligned_rows != 0 promises that every row of the student logits, the
+ * teacher logits and the gradient starts on a 16-byte boundary (base pointers
+ * and row strides in bytes are multiples of 16).  The size then covers the
+ * 16-byte vector path, which every call with such rows takes when vocab
+ * fills whole 16-byte vectors (vocab a multiple of 8 in bf16, of 4 in fp32).
+ * aligned_rows = 0 covers whichever path a call takes.  The two differ in the
+ * row kernel's exchange slots: at vocab = 151,936 in bf16, 96 bytes per token
+ * on the vector path (3 chunks per row) and 608 on the element-wise path (19
+ * chunks).  A call whose path needs more than the workspace it is given
+ * returns TURNKL_ERR_WORKSPACE and enqueues nothing.
+ *
+ * Returns 0 when the arguments are invalid (n_tokens < 0, vocab < 1, unknown
+ * dtype, max_turns < 1).  The workspace needs no initialisation; it must be
+ * 256-byte aligned.
  */
-size_t turnkl_workspace_bytes(int64_t n_tokens, int64_t vocab, int dtype, int32_t max_turns);
+size_t turnkl_workspace_bytes(int64_t n_tokens, int64_t vocab, int dtype, int32_t max_turns,
+                              int aligned_rows);
 
 /*
  * Fused forward + backward of the turn-blended reverse-KL loss.
@@ -223,6 +238,20 @@ int turnkl_fwd_bwd(const void* student_logits, int64_t ld_student, const void* t
  * token a padding-mask error, then a range error, then an ordering error,
  * then an outcome-flag error), or TURNKL_ERR_SYNC_TIMEOUT; TURNKL_ERR_HIP if
  * the read-back fails.
+ *
+ * TURNKL_ERR_SYNC_TIMEOUT.  The full-vocabulary row kernel splits a long row
+ * over several workgroups that exchange partial sums through the workspace;
+ * a workgroup waits for its row mates for a bounded number of polls (2^22,
+ * with a short sleep between polls: seconds of wall time).  The wait can only
+ * expire when the row mates cannot be scheduled, i.e. when other work holds
+ * the GPU's compute slots for that long.  Then every other workgroup that
+ * waits for a row mate gives up within 256 further polls (rows whose chunks
+ * all arrive are still computed, and discarded), the kernels after the row
+ * kernel skip their work, loss_out holds NaN, the gradient, the statistics
+ * and the per-token outputs are unspecified, and the workspace is ready for
+ * the next call.  The caller may simply repeat the call.  No other kernel of
+ * the call waits on another workgroup, and the top-K call never returns this
+ * code.
  */
 int turnkl_get_status(const void* workspace, hipStream_t stream);
 
@@ -246,41 +275,6 @@ double turnkl_alpha_schedule(int64_t k, int64_t K, double s, double e);
 
 /* Static description of a return code.  Host function. */
 const char* turnkl_status_string(int status);
-
-/*
- * Profiling hook for the calling host thread: while both events are non-NULL,
- * every turnkl_fwd_bwd call made by this thread records `before` immediately
- * before and `after` immediately after its row kernel (the kernel that reads
- * the logits and writes the gradient), on the call's stream.  Pass NULL, NULL
- * to stop.  The events must outlive the calls that record them.
- */
-int turnkl_profile_row_kernel(hipEvent_t before, hipEvent_t after);
-
-/*
- * Tiling override for the calling host thread.  The row kernel splits each
- * row of V logits into ceil(V / (256 * e * n)) balanced chunks, one
- * workgroup of 256 threads per chunk, where e is the number of elements in a
- * 16-byte vector (8 bf16, 4 fp32) and n = vectors_per_thread is the most
- * vectors a thread holds (1 to 25; default 25).  Smaller n means more, smaller
- * chunks per row.  0 restores the default.  The workspace size depends on it
- * (turnkl_workspace_bytes reads the same setting).  Results agree up to
- * floating-point summation order.  Returns TURNKL_ERR_INVALID_ARG for values
- * outside 0..25.
- */
-int turnkl_set_row_tiling(int vectors_per_thread);
-
-/*
- * Bound on the row kernel's wait for the partials of a row's other chunks,
- * for the calling host thread: a workgroup gives up after this many polls
- * that find a partial missing (s_sleep between polls), records
- * TURNKL_ERR_SYNC_TIMEOUT in the workspace and exits, and so does every
- * workgroup after it; the later kernels of the call see the error and skip
- * their work.  0 restores the default (2^22 polls, seconds).  The callers are
- * tests of that error path: a bound of 1 makes a batch of multi-chunk rows
- * time out at once while every kernel still exits normally.  Returns
- * TURNKL_ERR_INVALID_ARG for a negative value.
- */
-int turnkl_set_spin_limit(int polls);
 
 /* ------------------------------------------------------------------------
  * Top-K variant of the loss: the reverse KL on the teacher's top-K support
@@ -322,8 +316,8 @@ size_t turnkl_topk_workspace_bytes(int64_t n_tokens, int32_t k, int32_t max_turn
  * and teacher_vals.  Errors: as turnkl_fwd_bwd (TURNKL_ERR_ALIAS when either
  * gradient output overlaps an input or the other output), plus the device
  * error TURNKL_ERR_TOPK_ID for an id outside [0, vocab) in a supervised row.
- * The profiling hook of turnkl_profile_row_kernel brackets the two top-K
- * kernels (support rows, then the dense zero-fill and scatter).
+ * The profiling hook of turnkl_profile_row_kernel (turnkl_testing.h)
+ * brackets the top-K kernels (support rows, then the dense gradient).
  */
 int turnkl_fwd_bwd_topk(const void* student_logits, int64_t ld_student, int dtype,
                         int64_t n_tokens, int64_t vocab, const int32_t* teacher_ids,

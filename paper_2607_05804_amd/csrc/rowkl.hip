@@ -195,13 +195,38 @@ __device__ inline unsigned take_ticket(unsigned* counter) {
   return __builtin_amdgcn_atomic_inc32(counter, 0xFFFFFFFFu, __ATOMIC_RELAXED, "agent");
 }
 
-// Exchange word: the tag in the high half marks it written and says how the
-// chunk's partials are expressed (kTagFast / kTagOffset); value in the low half.
+// Exchange words.  A chunk's seven partials (M_s, S_s, A, M_t, S_t, C_a, C_b)
+// and its form tag (kTagFast / kTagOffset, how the partials are expressed)
+// travel as four 64-bit words, (M_s, S_s), (A, M_t), (S_t, C_a), (C_b, tag),
+// each published with one relaxed 64-bit atomic store and read back with
+// relaxed 64-bit atomic loads.  A partial is stored as the bits of v + 0 (so
+// -0 becomes +0) with the sign bit flipped, which is never zero; the slots
+// are cleared before the kernel, so a nonzero word is a published one.
 constexpr unsigned kTagFast = 1;
 constexpr unsigned kTagOffset = 2;
-__device__ inline unsigned long long tagged(float v, unsigned tag) {
-  return ((unsigned long long)tag << 32) | (unsigned long long)__float_as_uint(v);
+__device__ inline unsigned enc(float v) { return __float_as_uint(v + 0.0f) ^ 0x80000000u; }
+__device__ inline float dec(unsigned u) { return __uint_as_float(u ^ 0x80000000u); }
+__device__ inline unsigned long long word2(unsigned lo, unsigned hi) {
+  return ((unsigned long long)hi << 32) | (unsigned long long)lo;
 }
+// the seven partials of one chunk's four words, in publication order
+__device__ inline void unpack_partials(const unsigned long long* w, float (&out)[kPartials]) {
+#pragma unroll
+  for (int i = 0; i < kPartials; ++i) {
+    const unsigned long long x = w[i >> 1];
+    out[i] = dec((i & 1) ? (unsigned)(x >> 32) : (unsigned)x);
+  }
+}
+
+// The low half of the workspace's error key, read with a relaxed atomic
+// load: an error key's low nibble is a priority below 15, so the half equals
+// 0xFFFFFFFF exactly while no error has been recorded (a waiting workgroup
+// polls it to learn that another one has timed out).
+__device__ inline unsigned err_low(Header* hdr) {
+  return __hip_atomic_load(reinterpret_cast<unsigned*>(&hdr->err_key), __ATOMIC_RELAXED,
+                           __HIP_MEMORY_SCOPE_AGENT);
+}
+constexpr unsigned kNoErrorLow = 0xFFFFFFFFu;
 
 // Row merge.  A chunk reports (M_s, S_s, A, M_t, S_t, C_a, C_b) in one of two
 // forms:
@@ -284,8 +309,7 @@ __global__ __launch_bounds__(kRowThreads) void rowkl_kernel(RowParams p) {
 
   __shared__ float s_max[2][kRowWaves];
   __shared__ float s_sum[3][kRowWaves];
-  __shared__ float s_part[kMaxPartialWords];
-  __shared__ unsigned s_tag[kMaxChunks];
+  __shared__ unsigned long long s_word[kMaxChunks * kExchangeWords];
   __shared__ float s_ref[kRowWaves];
   __shared__ int s_lo[kMaxChunks + 1];  // first pack of each chunk
   __shared__ unsigned s_task;
@@ -593,23 +617,27 @@ __global__ __launch_bounds__(kRowThreads) void rowkl_kernel(RowParams p) {
       if (tid == 0) {
         const unsigned tag = offset ? kTagOffset : kTagFast;
         unsigned long long* mine = slot + c * kExchangeWords;
-        const float words[kExchangeWords] = {m2s, ss, aa, m2t, st, c_a, c_b};
+        const unsigned long long words[kExchangeWords] = {
+            word2(enc(m2s), enc(ss)), word2(enc(aa), enc(m2t)), word2(enc(st), enc(c_a)),
+            word2(enc(c_b), tag)};
 #pragma unroll
         for (int q = 0; q < kExchangeWords; ++q)
-          __hip_atomic_store(mine + q, tagged(words[q], tag), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+          __hip_atomic_store(mine + q, words[q], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
       }
+      // Wait for every word of the row, bounded: after spin_limit empty polls,
+      // or as soon as another workgroup of the call has timed out (checked
+      // every 256 polls), the task ends with the timeout error.
       for (int q = tid; q < nw; q += kRowThreads) {
         unsigned long long x;
         int spins = 0;
-        while (((x = __hip_atomic_load(slot + q, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT)) >> 32) == 0ull) {
-          if (++spins > p.spin_limit) {
+        while ((x = __hip_atomic_load(slot + q, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT)) == 0ull) {
+          if (++spins > p.spin_limit || ((spins & 255) == 0 && err_low(p.hdr) != kNoErrorLow)) {
             s_timeout = 1;
             break;
           }
           __builtin_amdgcn_s_sleep(2);
         }
-        s_part[q] = __uint_as_float((unsigned)x);
-        if (q % kExchangeWords == 0) s_tag[q / kExchangeWords] = (unsigned)(x >> 32);
+        s_word[q] = x;
       }
       __syncthreads();
       if (s_timeout) {
@@ -620,14 +648,16 @@ __global__ __launch_bounds__(kRowThreads) void rowkl_kernel(RowParams p) {
       // every thread merges all chunks in chunk order (uniform branches):
       // unrolled for the usual handful of chunks, a loop beyond
       constexpr int kUnrolled = 8;
-#define TURNKL_TAG(K) (__builtin_amdgcn_readfirstlane(s_tag[K]) == kTagOffset)
+#define TURNKL_TAG(K) \
+  (__builtin_amdgcn_readfirstlane((unsigned)(s_word[kExchangeWords * (K) + 3] >> 32)) == kTagOffset)
       r_s = -INFINITY;
       r_t = -INFINITY;
       row_offset = false;
 #define TURNKL_REFS(K)                                              \
   {                                                                 \
     const bool o = TURNKL_TAG(K);                                   \
-    const float* w = s_part + kExchangeWords * (K);                 \
+    float w[kPartials];                                             \
+    unpack_partials(s_word + kExchangeWords * (K), w);              \
     if (o && (!row_offset || w[5] > d_s)) {                         \
       d_s = w[5];                                                   \
       d_t = w[6];                                                   \
@@ -645,17 +675,25 @@ __global__ __launch_bounds__(kRowThreads) void rowkl_kernel(RowParams p) {
       const Float2 c_row = two_diff(d_s, d_t);
 #pragma unroll
       for (int k = 0; k < kUnrolled; ++k)
-        if (k < p.n_chunks) merge_chunk(TURNKL_TAG(k), s_part + kExchangeWords * k, r_s, r_t, c_row, r);
+        if (k < p.n_chunks) {
+          float w[kPartials];
+          unpack_partials(s_word + kExchangeWords * k, w);
+          merge_chunk(TURNKL_TAG(k), w, r_s, r_t, c_row, r);
+        }
 #pragma unroll 1
       for (int k = kUnrolled; k < p.n_chunks; ++k)
-        merge_chunk(TURNKL_TAG(k), s_part + kExchangeWords * k, r_s, r_t, c_row, r);
+      {
+        float w[kPartials];
+        unpack_partials(s_word + kExchangeWords * k, w);
+        merge_chunk(TURNKL_TAG(k), w, r_s, r_t, c_row, r);
+      }
 #undef TURNKL_TAG
     } else {
       r_s = natural_ref(offset, m2s);
       r_t = natural_ref(offset, m2t);
       d_s = c_a;
       d_t = c_b;
-      const float w[kExchangeWords] = {m2s, ss, aa, m2t, st, c_a, c_b};
+      const float w[kPartials] = {m2s, ss, aa, m2t, st, c_a, c_b};
       merge_chunk(offset, w, r_s, r_t, two_diff(d_s, d_t), r);
     }
     // without a gradient to write the task ends here

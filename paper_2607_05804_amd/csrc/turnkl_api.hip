@@ -8,10 +8,13 @@
 #include <initializer_list>
 
 #include "turnkl_internal.h"
+#include "turnkl_testing.h"
 
 namespace turnkl {
 
 namespace {
+// Measurement and test hooks (turnkl_testing.h), per host thread.  None of
+// them changes what turnkl_workspace_bytes returns.
 thread_local hipEvent_t t_row_before = nullptr;
 thread_local hipEvent_t t_row_after = nullptr;
 thread_local int t_vpt_override = 0;
@@ -28,9 +31,6 @@ constexpr int kDefaultVmax = 25;
 
 long long ceil_div(long long a, long long b) { return (a + b - 1) / b; }
 }  // namespace
-
-int thread_tiling_override() { return t_vpt_override; }
-int thread_spin_limit() { return t_spin_limit > 0 ? t_spin_limit : kDefaultSpinLimit; }
 
 // k = ceil(P / (256 * vmax)) chunks of a row of P packs, with boundaries
 // from chunk_start: 1 KiB-aligned when that keeps vpt = ceil(widest / 256)
@@ -85,14 +85,26 @@ RowTiling scalar_tiling(long long vocab) {
 
 namespace {
 
-// Exchange slots are sized for whichever path (vector or scalar) a call with
-// these sizes can take on this thread.
-int workspace_chunks(long long vocab, int dtype) {
-  const int a = vector_tiling(vocab, dtype, t_vpt_override).n_chunks;
-  const int b = scalar_tiling(vocab).n_chunks;
-  const int m = a > b ? a : b;
+// Whether a vocabulary admits the vector path at all (whole 16-byte packs, and
+// chunks long enough for the kernel's one-predicated-pack layout); a call then
+// takes it when its rows also start on 16-byte boundaries.
+bool vector_possible(const RowTiling& t, long long vocab) {
+  return vocab % t.epv == 0 && t.min_chunk >= (long long)kRowThreads * (t.vpt - 1);
+}
+
+// Chunks per row whose exchange slots a workspace holds (0: one chunk, no
+// slots): the vector path's when the caller promises aligned rows and the
+// vocabulary admits it, else the larger of the two paths'.
+int workspace_chunks(long long vocab, int dtype, bool aligned_rows, int vpt) {
+  const RowTiling v = vector_tiling(vocab, dtype, vpt);
+  const int sc = scalar_tiling(vocab).n_chunks;
+  int m = sc;
+  if (vector_possible(v, vocab)) m = aligned_rows ? v.n_chunks : (v.n_chunks > sc ? v.n_chunks : sc);
   return m > 1 ? m : 0;
 }
+
+size_t workspace_bytes_for(int64_t n_tokens, int64_t vocab, int dtype, int32_t max_turns,
+                           int aligned_rows, int vpt);
 
 bool overlaps(const void* a, size_t na, const void* b, size_t nb) {
   const char* pa = static_cast<const char*>(a);
@@ -170,26 +182,23 @@ int apply_options(const turnkl_options* o, long long n_tokens, int max_turns,
 // max_turns bounds: the statistics kernel runs 3 * max_turns + 1 workgroups.
 constexpr int kMaxTurns = (0x7FFFFFFF - 1) / 3;
 
-}  // namespace
-}  // namespace turnkl
-
-using namespace turnkl;
-
-extern "C" {
-
-size_t turnkl_workspace_bytes(int64_t n_tokens, int64_t vocab, int dtype, int32_t max_turns) {
+size_t workspace_bytes_for(int64_t n_tokens, int64_t vocab, int dtype, int32_t max_turns,
+                           int aligned_rows, int vpt) {
   if (n_tokens < 0 || vocab < 1 || max_turns < 1 || max_turns > kMaxTurns) return 0;
   if (dtype != TURNKL_BF16 && dtype != TURNKL_F32) return 0;
-  return make_layout(n_tokens, workspace_chunks(vocab, dtype), 0, max_turns).total;
+  if (vpt != 0 && !vpt_allowed(vpt)) return 0;
+  return make_layout(n_tokens, workspace_chunks(vocab, dtype, aligned_rows != 0, vpt), 0, max_turns)
+      .total;
 }
 
-int turnkl_fwd_bwd(const void* student_logits, int64_t ld_student, const void* teacher_logits,
-                   int64_t ld_teacher, int dtype, int64_t n_tokens, int64_t vocab,
-                   const int32_t* turn_id, const int32_t* traj_id, const uint8_t* loss_mask,
-                   double alpha, float grad_scale, float* loss_out, void* grad_out,
-                   int64_t ld_grad, turnkl_turn_stat* turn_stats_out, int32_t max_turns,
-                   int accumulate_stats, float* token_kl_out, const turnkl_options* options,
-                   void* workspace, size_t workspace_bytes, hipStream_t stream) {
+// The fused call on a caller workspace.
+int fwd_bwd_impl(const void* student_logits, int64_t ld_student, const void* teacher_logits,
+                 int64_t ld_teacher, int dtype, int64_t n_tokens, int64_t vocab,
+                 const int32_t* turn_id, const int32_t* traj_id, const uint8_t* loss_mask,
+                 double alpha, float grad_scale, float* loss_out, void* grad_out, int64_t ld_grad,
+                 turnkl_turn_stat* turn_stats_out, int32_t max_turns, int accumulate_stats,
+                 float* token_kl_out, const turnkl_options* options, void* workspace,
+                 size_t workspace_bytes, hipStream_t stream) {
   // ---- arguments
   if (dtype != TURNKL_BF16 && dtype != TURNKL_F32) return TURNKL_ERR_INVALID_ARG;
   if (n_tokens < 0 || n_tokens > 0x7FFFFFFFll || vocab < 1 || max_turns < 1 ||
@@ -220,10 +229,9 @@ int turnkl_fwd_bwd(const void* student_logits, int64_t ld_student, const void* t
   RowTiling tiling = vector_tiling(vocab, dtype, t_vpt_override);
   {
     const long long epv = tiling.epv;
-    bool ok = vocab % epv == 0 && ld_student % epv == 0 && ld_teacher % epv == 0;
+    bool ok = vector_possible(tiling, vocab) && ld_student % epv == 0 && ld_teacher % epv == 0;
     ok = ok && ((uintptr_t)student_logits & 15u) == 0 && ((uintptr_t)teacher_logits & 15u) == 0;
     if (grad_out) ok = ok && ld_grad % epv == 0 && ((uintptr_t)grad_out & 15u) == 0;
-    ok = ok && tiling.min_chunk >= (long long)kRowThreads * (tiling.vpt - 1);
     if (!ok) tiling = scalar_tiling(vocab);
   }
   if (tiling.n_chunks > kMaxChunks) return TURNKL_ERR_INVALID_ARG;
@@ -241,7 +249,8 @@ int turnkl_fwd_bwd(const void* student_logits, int64_t ld_student, const void* t
                              &sp, &ex))
     return rc;
 
-  const Layout L = make_layout(n_tokens, workspace_chunks(vocab, dtype), 0, max_turns);
+  // the layout of this call: exchange slots for the path it takes
+  const Layout L = make_layout(n_tokens, tiling.n_chunks > 1 ? tiling.n_chunks : 0, 0, max_turns);
   if (workspace_bytes < L.total) return TURNKL_ERR_WORKSPACE;
   Ws ws = bind(workspace, L);
   if (ex.weights) ws.w = ex.weights;
@@ -270,7 +279,7 @@ int turnkl_fwd_bwd(const void* student_logits, int64_t ld_student, const void* t
   rp.align = tiling.align;
   rp.bf16 = dtype == TURNKL_BF16;
   rp.lse = ex.lse;
-  rp.spin_limit = thread_spin_limit();
+  rp.spin_limit = t_spin_limit > 0 ? t_spin_limit : kDefaultSpinLimit;
   const bool prof = t_row_before && t_row_after;
   if (prof && hipEventRecord(t_row_before, stream) != hipSuccess) return TURNKL_ERR_HIP;
   if (launch_rows(rp, tiling, stream) != hipSuccess) return TURNKL_ERR_HIP;
@@ -280,6 +289,37 @@ int turnkl_fwd_bwd(const void* student_logits, int64_t ld_student, const void* t
                     accumulate_stats, stream) != hipSuccess)
     return TURNKL_ERR_HIP;
   return TURNKL_OK;
+}
+
+}  // namespace
+}  // namespace turnkl
+
+using namespace turnkl;
+
+extern "C" {
+
+size_t turnkl_workspace_bytes(int64_t n_tokens, int64_t vocab, int dtype, int32_t max_turns,
+                              int aligned_rows) {
+  return workspace_bytes_for(n_tokens, vocab, dtype, max_turns, aligned_rows, 0);
+}
+
+size_t turnkl_testing_workspace_bytes(int64_t n_tokens, int64_t vocab, int dtype,
+                                      int32_t max_turns, int aligned_rows,
+                                      int vectors_per_thread) {
+  return workspace_bytes_for(n_tokens, vocab, dtype, max_turns, aligned_rows, vectors_per_thread);
+}
+
+int turnkl_fwd_bwd(const void* student_logits, int64_t ld_student, const void* teacher_logits,
+                   int64_t ld_teacher, int dtype, int64_t n_tokens, int64_t vocab,
+                   const int32_t* turn_id, const int32_t* traj_id, const uint8_t* loss_mask,
+                   double alpha, float grad_scale, float* loss_out, void* grad_out,
+                   int64_t ld_grad, turnkl_turn_stat* turn_stats_out, int32_t max_turns,
+                   int accumulate_stats, float* token_kl_out, const turnkl_options* options,
+                   void* workspace, size_t workspace_bytes, hipStream_t stream) {
+  return fwd_bwd_impl(student_logits, ld_student, teacher_logits, ld_teacher, dtype, n_tokens,
+                      vocab, turn_id, traj_id, loss_mask, alpha, grad_scale, loss_out, grad_out,
+                      ld_grad, turn_stats_out, max_turns, accumulate_stats, token_kl_out, options,
+                      workspace, workspace_bytes, stream);
 }
 
 size_t turnkl_topk_workspace_bytes(int64_t n_tokens, int32_t k, int32_t max_turns) {

@@ -81,8 +81,11 @@ struct Layout {
 
 inline size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
 
-// 64-bit words a row-kernel chunk publishes to its row mates
-constexpr int kExchangeWords = 7;
+// A row-kernel chunk reports seven fp32 partials to its row mates, packed two
+// to a 64-bit word with a tag in the last half: four words per chunk, each
+// published with one 64-bit atomic store (see rowkl.hip, "Exchange words").
+constexpr int kPartials = 7;
+constexpr int kExchangeWords = 4;
 
 // n_chunks > 1: exchange slots of the full-vocabulary row kernel; topk_k > 0:
 // the top-K path's staging of the scaled gradient on each row's support;
@@ -177,8 +180,7 @@ inline Ws bind(void* base, const Layout& L) {
 constexpr int kRowThreads = 256;
 constexpr int kScalarVpt = 32;         // elements per thread on the unaligned path
 constexpr int kMaxVpt = 25;            // packs per thread of the widest vector instantiation
-constexpr int kMaxChunks = 128;                 // chunks per row
-constexpr int kMaxPartialWords = kMaxChunks * kExchangeWords;  // LDS words for exchanged partials
+constexpr int kMaxChunks = 128;        // chunks per row
 
 struct RowTiling {
   bool vector;  // 16-byte vector loads (aligned rows, vocab a multiple of the vector)
@@ -207,7 +209,6 @@ __host__ __device__ inline long long chunk_start(long long n_packs, int n_chunks
 // Tiling of the vector path for a given vectors-per-thread (0 = automatic).
 RowTiling vector_tiling(long long vocab, int dtype, int vpt);
 RowTiling scalar_tiling(long long vocab);
-int thread_tiling_override();
 
 // ---------------------------------------------------------------------------
 // launches (each returns hipSuccess or the launch error)
@@ -283,9 +284,9 @@ struct RowParams {
   float* lse;    // [n_rows][2] log-partition functions of both rows, or null
 };
 
-// Default bound on those polls (with s_sleep between them: seconds).
+// Default bound on those polls (s_sleep between polls; every 256th poll also
+// checks whether another workgroup of the call has already timed out).
 constexpr int kDefaultSpinLimit = 1 << 22;
-int thread_spin_limit();
 
 hipError_t launch_rows(const RowParams& p, const RowTiling& t, hipStream_t s);
 

@@ -9,6 +9,7 @@ from __future__ import annotations
 
 import ctypes
 import os
+import threading
 
 import numpy as np
 import torch
@@ -32,19 +33,24 @@ BF16 = 0
 F32 = 1
 
 # Names of every entry point include/turnkl.h declares.
-EXPORTS = ("turnkl_workspace_bytes", "turnkl_fwd_bwd", "turnkl_get_status",
-           "turnkl_get_segments", "turnkl_alpha_schedule", "turnkl_status_string",
-           "turnkl_profile_row_kernel", "turnkl_set_row_tiling", "turnkl_set_spin_limit",
-           "turnkl_topk_workspace_bytes", "turnkl_fwd_bwd_topk",
+EXPORTS = ("turnkl_workspace_bytes", "turnkl_fwd_bwd", "turnkl_get_status", "turnkl_get_segments", "turnkl_alpha_schedule",
+           "turnkl_status_string", "turnkl_topk_workspace_bytes", "turnkl_fwd_bwd_topk",
            "turnkl_depth_default_config", "turnkl_depth_init", "turnkl_depth_plan",
            "turnkl_depth_update", "turnkl_loss_share", "turnkl_budget_report",
            "turnkl_outcome_gap")
+# ... and every entry point include/turnkl_testing.h declares (measurement and
+# test hooks).
+TESTING_EXPORTS = ("turnkl_profile_row_kernel", "turnkl_set_row_tiling",
+                   "turnkl_testing_workspace_bytes", "turnkl_set_spin_limit")
 
 STAT_DTYPE = np.dtype([("n_tokens", "<i8"), ("n_traj", "<i8"), ("kl_mean", "<f8"),
                        ("kl_m2", "<f8"), ("kl_var", "<f8"), ("loss_mass", "<f8")])
 STAT_FIELDS = 6  # int64, int64, 4 x float64 -> 48 bytes
 
 _lib = None
+# The tiling override of turnkl_set_row_tiling is per host thread in the
+# library; this mirror lets the binding size workspaces for it.
+_thread = threading.local()
 
 
 class Options(ctypes.Structure):
@@ -94,7 +100,10 @@ def lib() -> ctypes.CDLL:
         l = ctypes.CDLL(LIB_PATH)
         c = ctypes
         l.turnkl_workspace_bytes.restype = c.c_size_t
-        l.turnkl_workspace_bytes.argtypes = [c.c_int64, c.c_int64, c.c_int, c.c_int32]
+        l.turnkl_workspace_bytes.argtypes = [c.c_int64, c.c_int64, c.c_int, c.c_int32, c.c_int]
+        l.turnkl_testing_workspace_bytes.restype = c.c_size_t
+        l.turnkl_testing_workspace_bytes.argtypes = [c.c_int64, c.c_int64, c.c_int, c.c_int32,
+                                                     c.c_int, c.c_int]
         l.turnkl_fwd_bwd.restype = c.c_int
         l.turnkl_fwd_bwd.argtypes = [
             c.c_void_p, c.c_int64, c.c_void_p, c.c_int64, c.c_int, c.c_int64, c.c_int64,
@@ -154,14 +163,24 @@ def alpha_schedule(k: int, K: int, s: float = 0.0, e: float = 1.0) -> float:
     return float(lib().turnkl_alpha_schedule(k, K, s, e))
 
 
-def workspace_bytes(n_tokens: int, vocab: int, dtype: int, max_turns: int) -> int:
-    return int(lib().turnkl_workspace_bytes(n_tokens, vocab, dtype, max_turns))
+def workspace_bytes(n_tokens: int, vocab: int, dtype: int, max_turns: int,
+                    aligned_rows: bool = True) -> int:
+    """turnkl_workspace_bytes; under a tiling override of this thread
+    (set_row_tiling), turnkl_testing_workspace_bytes for that tiling."""
+    vpt = getattr(_thread, "vpt", 0)
+    if vpt:
+        return int(lib().turnkl_testing_workspace_bytes(n_tokens, vocab, dtype, max_turns,
+                                                        int(bool(aligned_rows)), vpt))
+    return int(lib().turnkl_workspace_bytes(n_tokens, vocab, dtype, max_turns,
+                                            int(bool(aligned_rows))))
 
 
 def set_row_tiling(vectors_per_thread: int) -> None:
+    """Tiling override for this thread (turnkl_testing.h); 0 restores the default."""
     rc = lib().turnkl_set_row_tiling(vectors_per_thread)
     if rc != OK:
         raise TurnKLError(rc, "turnkl_set_row_tiling")
+    _thread.vpt = int(vectors_per_thread)
 
 
 def set_spin_limit(polls: int) -> None:
@@ -246,11 +265,27 @@ def _check_common(student, n, max_turns, turn_id, traj_id, loss_mask, turn_stats
             raise ValueError("grad must match the student logits' device, dtype and shape")
 
 
-class Workspace:
-    """Caller-owned device scratch for turnkl_fwd_bwd (a uint8 torch tensor)."""
+def _rows_aligned(*tensors) -> bool:
+    """Whether every row of these logit or gradient matrices starts on a
+    16-byte boundary (base address and row stride in bytes)."""
+    for t in tensors:
+        if t is None or t.dim() != 2 or t.shape[0] == 0:
+            continue
+        if t.data_ptr() % 16 or (t.stride(0) * t.element_size()) % 16:
+            return False
+    return True
 
-    def __init__(self, n_tokens: int, vocab: int, dtype: int, max_turns: int, device="cuda"):
-        nbytes = workspace_bytes(n_tokens, vocab, dtype, max_turns)
+
+class Workspace:
+    """Caller-owned device scratch for turnkl_fwd_bwd (a uint8 torch tensor).
+
+    aligned_rows: the calls it serves pass logit and gradient rows that start
+    on 16-byte boundaries (turnkl_workspace_bytes); False sizes it for any
+    rows."""
+
+    def __init__(self, n_tokens: int, vocab: int, dtype: int, max_turns: int, device="cuda",
+                 aligned_rows: bool = True):
+        nbytes = workspace_bytes(n_tokens, vocab, dtype, max_turns, aligned_rows)
         if nbytes == 0:
             raise TurnKLError(ERR_INVALID_ARG, "turnkl_workspace_bytes")
         self.tensor = torch.empty(nbytes, dtype=torch.uint8, device=device)
@@ -273,6 +308,32 @@ class Workspace:
         k = n_seg.value
         names = ("start", "length", "traj", "turn", "n_sup")
         return {nm: b[:k].cpu().numpy().astype(np.int64) for nm, b in zip(names, bufs)}
+
+
+def _check_fused_inputs(student, teacher, turn_id, traj_id, loss_mask):
+    """dtype code, n_tokens and vocab of a fused call, after checking its inputs."""
+    dt = _dtype_code(student)
+    if teacher.dtype != student.dtype:
+        raise TypeError("student and teacher logits must share a dtype")
+    if teacher.shape != student.shape or teacher.device != student.device:
+        raise ValueError("student and teacher logits must share a shape and a device")
+    n, v = (int(student.shape[0]), int(student.shape[1])) if student.dim() == 2 else (0, 0)
+    for t in (turn_id, traj_id):
+        if t.dtype != torch.int32 or t.numel() != n:
+            raise ValueError("turn_id / traj_id must be int32 with one entry per row")
+    if loss_mask.dtype != torch.uint8 or loss_mask.numel() != n:
+        raise ValueError("loss_mask must be uint8 with one entry per row")
+    return dt, n, v
+
+
+def _fused_args(student, teacher, dt, n, v, turn_id, traj_id, loss_mask, alpha, grad_scale,
+                loss, grad_t, turn_stats, max_turns, accumulate_stats, kl_t, options):
+    """turnkl_fwd_bwd's arguments before the workspace, in order."""
+    return [_ptr(student), _row_stride(student) if n else v, _ptr(teacher),
+            _row_stride(teacher) if n else v, dt, n, v, _ptr(turn_id), _ptr(traj_id),
+            _ptr(loss_mask), float(alpha), float(grad_scale), _ptr(loss), _ptr(grad_t),
+            (_row_stride(grad_t) if n else v) if grad_t is not None else 0, _ptr(turn_stats),
+            int(max_turns), int(bool(accumulate_stats)), _ptr(kl_t), options]
 
 
 def fwd_bwd(student: torch.Tensor, teacher: torch.Tensor, turn_id: torch.Tensor,
@@ -299,17 +360,7 @@ def fwd_bwd(student: torch.Tensor, teacher: torch.Tensor, turn_id: torch.Tensor,
     unsupervised tokens).  Returns (loss[3] tensor, grad or None, turn_stats or
     None, token_kl or None, workspace).
     """
-    dt = _dtype_code(student)
-    if teacher.dtype != student.dtype:
-        raise TypeError("student and teacher logits must share a dtype")
-    if teacher.shape != student.shape or teacher.device != student.device:
-        raise ValueError("student and teacher logits must share a shape and a device")
-    n, v = (int(student.shape[0]), int(student.shape[1])) if student.dim() == 2 else (0, 0)
-    for t in (turn_id, traj_id):
-        if t.dtype != torch.int32 or t.numel() != n:
-            raise ValueError("turn_id / traj_id must be int32 with one entry per row")
-    if loss_mask.dtype != torch.uint8 or loss_mask.numel() != n:
-        raise ValueError("loss_mask must be uint8 with one entry per row")
+    dt, n, v = _check_fused_inputs(student, teacher, turn_id, traj_id, loss_mask)
     dev = student.device
     if isinstance(grad, str):
         if grad == "new":
@@ -321,7 +372,8 @@ def fwd_bwd(student: torch.Tensor, teacher: torch.Tensor, turn_id: torch.Tensor,
     else:
         grad_t = grad
     if workspace is None:
-        workspace = Workspace(n, v, dt, max_turns, device=dev)
+        workspace = Workspace(n, v, dt, max_turns, device=dev,
+                              aligned_rows=_rows_aligned(student, teacher, grad_t))
     loss = torch.empty(3, dtype=torch.float32, device=dev)
     if isinstance(token_kl, torch.Tensor):
         kl_t = token_kl
@@ -330,16 +382,12 @@ def fwd_bwd(student: torch.Tensor, teacher: torch.Tensor, turn_id: torch.Tensor,
     _check_common(student, n, max_turns, turn_id, traj_id, loss_mask, turn_stats, outcome_stats,
                   kl_t, grad_t)
     stream = torch.cuda.current_stream(dev).cuda_stream
+    opts = _options(n, support_floor, support_frac, success, outcome_stats, token_weights,
+                    token_lse, dev)
     rc = lib().turnkl_fwd_bwd(
-        _ptr(student), _row_stride(student) if n else v, _ptr(teacher),
-        _row_stride(teacher) if n else v, dt, n, v, _ptr(turn_id), _ptr(traj_id), _ptr(loss_mask),
-        float(alpha), float(grad_scale), _ptr(loss), _ptr(grad_t),
-        (_row_stride(grad_t) if n else v) if grad_t is not None else 0, _ptr(turn_stats),
-        int(max_turns), int(bool(accumulate_stats)), _ptr(kl_t),
-        _options(n, support_floor, support_frac, success, outcome_stats, token_weights, token_lse,
-                 dev),
-        _ptr(workspace.tensor),
-        workspace.nbytes, ctypes.c_void_p(stream))
+        *_fused_args(student, teacher, dt, n, v, turn_id, traj_id, loss_mask, alpha, grad_scale,
+                     loss, grad_t, turn_stats, max_turns, accumulate_stats, kl_t, opts),
+        _ptr(workspace.tensor), workspace.nbytes, ctypes.c_void_p(stream))
     if rc != OK:
         raise TurnKLError(rc, "turnkl_fwd_bwd")
     if check:

@@ -11,10 +11,11 @@ from paper_2607_05804_amd import turnkl as T
 
 ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
 HEADER = os.path.join(ROOT, "include", "turnkl.h")
+TESTING_HEADER = os.path.join(ROOT, "include", "turnkl_testing.h")
 
 
-def declared_functions():
-    src = open(HEADER).read()
+def declared_functions(path=HEADER):
+    src = open(path).read()
     src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
     return sorted(set(re.findall(r"\b(turnkl_[a-z_]+)\s*\(", src)))
 
@@ -22,8 +23,11 @@ def declared_functions():
 def test_every_declared_symbol_is_exported():
     names = declared_functions()
     assert set(names) == set(T.EXPORTS), names
+    testing = declared_functions(TESTING_HEADER)
+    assert set(testing) == set(T.TESTING_EXPORTS), testing
+    assert not set(names) & set(testing)  # the product header declares no test hook
     lib = ctypes.CDLL(T.LIB_PATH)
-    for n in names:
+    for n in names + testing:
         assert hasattr(lib, n), n
 
 
@@ -39,6 +43,37 @@ def test_status_strings_and_alpha_schedule():
     assert T.alpha_schedule(5, 10, 0.6, 0.6) == 0.0 and T.alpha_schedule(6, 10, 0.6, 0.6) == 1.0
     import math
     assert math.isnan(T.alpha_schedule(1, 0))
+
+
+def _ws(n, v, dtype, max_turns, aligned):
+    return int(T.lib().turnkl_workspace_bytes(n, v, dtype, max_turns, aligned))
+
+
+def test_workspace_bytes_sized_for_the_path_the_call_takes():
+    """With aligned rows the workspace holds the 16-byte vector path's
+    exchange slots only (4 words of 8 bytes per chunk, 3 chunks per row at
+    V = 151,936 in bf16); without, also the element-wise path's (19 chunks).
+    The size is a pure function of the arguments: a tiling override of the
+    calling thread changes only turnkl_testing_workspace_bytes."""
+    n, v = 65536, 151936
+    aligned, unaligned = _ws(n, v, T.BF16, 50, 1), _ws(n, v, T.BF16, 50, 0)
+    assert aligned <= 15_000_000  # the long-horizon batch's workspace
+    assert unaligned - aligned == n * (19 - 3) * 32
+    # a vocabulary without whole 16-byte vectors only ever takes the element-wise path
+    assert _ws(n, v + 1, T.BF16, 50, 1) == _ws(n, v + 1, T.BF16, 50, 0)
+    # one chunk per row: no slots on either path
+    assert _ws(1000, 1024, T.BF16, 8, 1) == _ws(1000, 1024, T.BF16, 8, 0)
+    lib = T.lib()
+    T.set_row_tiling(3)
+    try:
+        assert _ws(n, v, T.BF16, 50, 1) == aligned
+        t = int(lib.turnkl_testing_workspace_bytes(n, v, T.BF16, 50, 1, 3))
+        assert t == aligned + n * (25 - 3) * 32  # 3 packs per thread: 25 chunks per row
+        assert T.workspace_bytes(n, v, T.BF16, 50) == t  # the binding follows the override
+    finally:
+        T.set_row_tiling(0)
+    assert int(lib.turnkl_testing_workspace_bytes(n, v, T.BF16, 50, 1, 0)) == aligned
+    assert int(lib.turnkl_testing_workspace_bytes(n, v, T.BF16, 50, 1, 26)) == 0
 
 
 def test_workspace_bytes():
@@ -76,7 +111,8 @@ def _call(**kw):
     es = 2 if kw.get("dtype", T.BF16) == T.BF16 else 4
     zs = kw.get("zs", 0x100000000)
     zt = kw.get("zt", 0x200000000)
-    ws_bytes = T.workspace_bytes(n, v, kw.get("dtype", T.BF16), kw.get("max_turns", 8))
+    ws_bytes = T.workspace_bytes(n, v, kw.get("dtype", T.BF16), kw.get("max_turns", 8),
+                                 kw.pop("aligned", True))
     args = dict(zs=zs, ld_s=v, zt=zt, ld_t=v, dtype=T.BF16, n=n, v=v, turn=0x300000000,
                 traj=0x300100000, mask=0x300200000, alpha=0.5, scale=1.0, loss=0x300300000,
                 grad=0x400000000, ld_g=v, stats=0, max_turns=8, acc=0, kl=0,
@@ -127,9 +163,13 @@ def _opts(o):
     (dict(grad=0x100000000 + 2), T.ERR_ALIAS),
     (dict(grad=0x100000000, ld_g=2048), T.ERR_ALIAS),
     (dict(grad=0x100000000 - 2 * 1024), T.ERR_ALIAS),
-    # workspace too small or misaligned
+    # workspace too small or misaligned; sized for aligned rows but given a
+    # row stride that is not a whole number of 16-byte vectors (the
+    # element-wise path, 19 chunks per row instead of 3)
     (dict(ws_bytes=1024), T.ERR_WORKSPACE),
     (dict(ws=0x500000010), T.ERR_WORKSPACE),
+    (dict(v=151936, ld_s=151937, ld_t=151936, ld_g=151936), T.ERR_WORKSPACE),
+    (dict(v=151936, ld_s=151936, ld_t=151936, ld_g=151936, zt=0x200000002), T.ERR_WORKSPACE),
     (dict(max_turns=(2**31 - 2) // 3 + 1), T.ERR_INVALID_ARG),
     # size limits: 128 chunks per row on the vector path (25 packs of 8 bf16 per
     # thread) and on the scalar path (32 elements per thread), 32-bit row
@@ -164,6 +204,16 @@ def _opts(o):
 ])
 def test_host_rejects_bad_arguments_before_launch(kw, code):
     assert _call(**kw) == code
+
+
+def test_unaligned_rows_run_with_a_workspace_sized_for_them():
+    """The same unaligned call is accepted by the host checks once the
+    workspace is sized with aligned_rows = 0 (it then fails only at the first
+    HIP call: a launch error, since the fake addresses are never reached on a
+    machine without a GPU)."""
+    kw = dict(v=151936, ld_s=151937, ld_t=151936, ld_g=151936)
+    assert _call(**kw) == T.ERR_WORKSPACE
+    assert _call(aligned=False, **kw) not in (T.ERR_WORKSPACE, T.ERR_INVALID_ARG, T.ERR_ALIAS)
 
 
 def test_binding_fails_loudly_without_library(monkeypatch, tmp_path):
@@ -233,7 +283,7 @@ def test_topk_host_rejects_bad_arguments_before_launch(kw, code):
 
 
 def test_header_is_plain_c_and_links(tmp_path):
-    """include/turnkl.h compiles as C11 with warnings as errors, and a C
+    """include/turnkl.h (and turnkl_testing.h) compile as C11 with warnings as errors, and a C
     program linked against the library calls its host entry points (no GPU
     is touched)."""
     import shutil
@@ -245,8 +295,10 @@ def test_header_is_plain_c_and_links(tmp_path):
     src.write_text(r'''
 #include <stdio.h>
 #include "turnkl.h"
+#include "turnkl_testing.h"
 int main(void) {
-  size_t b = turnkl_workspace_bytes(1000, 151936, TURNKL_BF16, 50);
+  size_t b = turnkl_workspace_bytes(1000, 151936, TURNKL_BF16, 50, 1);
+  if (turnkl_testing_workspace_bytes(1000, 151936, TURNKL_BF16, 50, 1, 0) != b) return 3;
   turnkl_depth_config c;
   turnkl_depth_default_config(&c);
   if (b == 0 || c.h_max < c.h_min) return 1;
