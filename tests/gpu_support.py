@@ -171,3 +171,68 @@ def rows_bits_to_host(t: torch.Tensor, rows) -> np.ndarray:
 def device_row_source(zs: torch.Tensor, zt: torch.Tensor):
     """Oracle row source reading the generator's output from device memory."""
     return lambda rows: (rows_bits_to_host(zs, rows), rows_bits_to_host(zt, rows))
+
+
+def ticket_order_rows(mask: np.ndarray, n_ends: int = 100, n_random: int = 800, seed: int = 0):
+    """Supervised rows for a full-size gradient comparison: the first and the
+    last n_ends supervised rows (the two ends of the row kernel's row-major
+    ticket order) and n_random others.  Every row covers all of its chunks."""
+    rng = np.random.default_rng(seed)
+    sup = np.nonzero(np.asarray(mask))[0]
+    pick = set(int(x) for x in sup[:n_ends]) | set(int(x) for x in sup[-n_ends:])
+    rest = np.setdiff1d(sup, np.fromiter(pick, np.int64, len(pick)))
+    if rest.size:
+        pick |= set(int(x) for x in rng.choice(rest, size=min(n_random, rest.size), replace=False))
+    return sorted(pick)
+
+
+def check_grad_rows_batched(grad_dev: torch.Tensor, w: np.ndarray, grad_scale: float, rows,
+                            host_rows, dtype: int, batch: int = 128) -> float:
+    """check_grad_rows on many rows with bounded host memory: the oracle's
+    unweighted row gradients are computed batch by batch from host copies of
+    the logit rows, host_rows(rows) -> (zs, zt), and compared with the device
+    rows.  Returns the worst unweighted absolute error."""
+    rows = np.asarray(sorted(rows), np.int64)
+    worst = 0.0
+    bf16 = grad_dev.dtype == torch.bfloat16
+    for k0 in range(0, rows.shape[0], batch):
+        r = rows[k0:k0 + batch]
+        zs, zt = host_rows(r)
+        _, g_ref = O.row_kl(zs, zt, dtype, want_grad=True)
+        G = rows_to_host(grad_dev, r).astype(np.float64)
+        scale = grad_scale * np.asarray(w)[r]
+        assert np.all(scale != 0.0)
+        err = np.abs(G / scale[:, None] - g_ref)
+        worst = max(worst, float(err.max()))
+        assert err.max() <= 2e-2, (k0, err.max())
+        bound = (2.0 ** -8 * np.abs(g_ref) + 2e-5) if bf16 else (1e-4 * np.abs(g_ref) + 2e-6)
+        bad = np.argwhere(err > bound)
+        assert bad.size == 0, (r[bad[:5, 0]], bad[:5, 1], err[tuple(bad[:5].T)])
+    return worst
+
+
+def check_grad_every_row_on_device(grad_dev: torch.Tensor, mask: np.ndarray, w: np.ndarray,
+                                   grad_scale: float, block: int = 4096) -> None:
+    """Properties every gradient row must have, checked on the device over
+    all rows in blocks: each unsupervised row is exactly zero (in place, that
+    proves the row's student logits were overwritten), and each supervised
+    row sums to zero, as dKL/dz_s does (sum_v p_s(v) (d_v - KL) = 0), up to
+    the rounding of its stored elements: |sum_v G| <= 2^-8 sum_v |G| +
+    1e-6 |grad_scale w_i|."""
+    dev = grad_dev.device
+    mask = np.asarray(mask)
+    uns = np.nonzero(mask == 0)[0]
+    for k0 in range(0, uns.shape[0], block):
+        idx = torch.from_numpy(uns[k0:k0 + block]).to(dev)
+        nz = int(torch.count_nonzero(grad_dev.index_select(0, idx)).item())
+        assert nz == 0, ("unsupervised rows with nonzero gradient", k0, nz)
+    sup = np.nonzero(mask)[0]
+    for k0 in range(0, sup.shape[0], block):
+        r = sup[k0:k0 + block]
+        g = grad_dev.index_select(0, torch.from_numpy(r).to(dev)).float()
+        s = g.sum(dim=1).double().cpu().numpy()
+        a = g.abs().sum(dim=1).double().cpu().numpy()
+        del g
+        floor = 1e-6 * np.abs(grad_scale * np.asarray(w)[r])
+        bad = np.nonzero(np.abs(s) > 2.0 ** -8 * a + floor)[0]
+        assert bad.size == 0, ("row sums", r[bad[:5]], s[bad[:5]], a[bad[:5]])
