@@ -43,7 +43,7 @@ def row_kernel_digest() -> str:
 
 
 WORKLOAD_NAMES = {"long_horizon": "long-horizon agent batch", "peaked": "peaked-teacher batch",
-                  "stress": "stress batch"}
+                  "stress": "stress batch", "agent": "agent batch"}
 
 
 def committed_traffic():
@@ -398,7 +398,11 @@ def main() -> int:
                          "(bandwidth context and counter calibration)")
     ap.add_argument("--workload", default="long_horizon", choices=sorted(WORKLOAD_NAMES),
                     help="the batch to time (the default is the headline batch; the others "
-                         "are the full-size parity batches, 16,534 and 131,072 tokens)")
+                         "are the parity batches: peaked 16,534 tokens, stress 131,072 tokens "
+                         "with the gradient in place, agent 4,480 tokens at V = 32,000)")
+    ap.add_argument("--out-of-place", action="store_true",
+                    help="write the stress batch's gradient to a separate buffer instead of "
+                         "over the student logits")
     ap.add_argument("--sustain", type=float, default=0.0, metavar="SECONDS",
                     help="instead of the measurements, run the timed call back to back for "
                          "this long and report its rate (for clock and power readings under "
@@ -428,7 +432,12 @@ def main() -> int:
     turn = torch.from_numpy(w.turn_id).to(dev)
     traj = torch.from_numpy(w.traj_id).to(dev)
     mask = torch.from_numpy(w.loss_mask).to(dev)
-    grad = torch.empty_like(zs)
+    # The stress batch writes its gradient over the student logits.  Every
+    # timed call then needs the original logits back: a device-to-device copy
+    # from a pristine copy, made before the call's events are recorded.
+    in_place = w.in_place and not args.out_of_place
+    pristine = zs.clone() if in_place else None
+    grad = zs if in_place else torch.empty_like(zs)
     stats = T.new_turn_stats(w.max_turns, device=dev)
     kl = torch.empty(n, dtype=torch.float32, device=dev)
     ws = T.Workspace(n, V, T.BF16, w.max_turns, device=dev)
@@ -437,24 +446,35 @@ def main() -> int:
         return T.fwd_bwd(zs, zt, turn, traj, mask, alpha, grad=grad, max_turns=w.max_turns,
                          turn_stats=stats, token_kl=kl, workspace=ws, check=False)
 
+    def restore():
+        if in_place:
+            zs.copy_(pristine)
+
     for _ in range(args.warmup):
+        restore()
         step()
     torch.cuda.synchronize()
     if ws.status() != T.OK:
         raise RuntimeError(T.status_string(ws.status()))
     if args.sustain > 0:
+        if in_place:
+            raise SystemExit("--sustain times the out-of-place call (add --out-of-place)")
         return sustain(T, step, ws, n, args.sustain)
 
-    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
-          for _ in range(args.steps)]
-    for a, b in ev:  # materialise the events before the timed region
-        a.record()
-        b.record()
+    mk = lambda: torch.cuda.Event(enable_timing=True)
+    ev = [(mk(), mk()) for _ in range(args.steps)]     # around the row kernel
+    call = [(mk(), mk()) for _ in range(args.steps)]   # around the whole call
+    for e in ev + call:  # materialise the events before the timed region
+        e[0].record()
+        e[1].record()
     torch.cuda.synchronize()
     t0 = time.perf_counter()
-    for a, b in ev:
+    for (a, b), (ca, cb) in zip(ev, call):
+        restore()
+        ca.record()
         T.profile_row_kernel(a, b)
         step()
+        cb.record()
     T.profile_row_kernel(None, None)
     torch.cuda.synchronize()
     elapsed = time.perf_counter() - t0
@@ -462,8 +482,11 @@ def main() -> int:
         raise RuntimeError(T.status_string(ws.status()))
 
     row_all = np.array([a.elapsed_time(b) for a, b in ev])
+    call_all = np.array([a.elapsed_time(b) for a, b in call])
     row_ms = float(row_all.mean())
-    ms_per_step = elapsed * 1e3 / args.steps
+    # in place, the wall clock also holds the restoring copies: the step time
+    # is then the calls' own duration from their events
+    ms_per_step = float(call_all.mean()) if in_place else elapsed * 1e3 / args.steps
     es = 2
     row_bytes = n_sup * 3 * V * es + (n - n_sup) * V * es
     achieved = row_bytes / (row_ms * 1e-3) / 1e9
@@ -471,7 +494,7 @@ def main() -> int:
     traffic = committed_traffic() if args.workload == "long_horizon" else None
     out = {
         "metric": "fused turn-KL fwd+bwd tokens/sec and achieved HBM GB/s (% of peak), V=151936",
-        "value": n * args.steps / elapsed,
+        "value": n / (ms_per_step * 1e-3),
         "unit": "tokens/s",
         "n_gpus": 1,
         "steps": args.steps,
@@ -487,7 +510,10 @@ def main() -> int:
                         f"{int(w.traj_id.max()) + 1} trajectories, "
                         f"{round(100 * (1 - n_sup / n))}% of tokens masked, alpha={alpha}",
             "n_tokens": n, "vocab": V, "supervised_tokens": n_sup, "logits": "bf16",
-            "gradient": "bf16, out of place", "parallelism": "single GPU",
+            "gradient": ("bf16, in place over the student logits (restored from a pristine "
+                         "device copy before each call, outside the call's events)"
+                         if in_place else "bf16, out of place"),
+            "parallelism": "single GPU", "workspace_bytes": ws.nbytes,
         },
         "roofline": {
             "bound": "hbm",
@@ -504,24 +530,32 @@ def main() -> int:
             "algorithmic_bytes_per_launch": row_bytes,
         },
         "step_hbm_gbs": row_bytes / (ms_per_step * 1e-3) / 1e9,
-        "supervised_tokens_per_s": n_sup * args.steps / elapsed,
+        "supervised_tokens_per_s": n_sup / (ms_per_step * 1e-3),
+        "call_ms_median": float(np.median(call_all)),
+        "wall_ms_per_step": elapsed * 1e3 / args.steps,
     }
-    out["graph_replay"] = graph_timing(T, step, ws, args.steps)
-    out["depth_controller"] = depth_controller_timing(T, stats, w)
     stats_np = T.read_turn_stats(stats)
-    out["floor_and_outcome"] = options_timing(T, zs, zt, turn, traj, mask, w, grad, args.steps,
-                                              args.warmup)
-    out["all_supervised"] = all_supervised_timing(T, zs, zt, turn, traj, w, grad, args.steps,
-                                                  args.warmup)
-    del grad
-    torch.cuda.empty_cache()
-    out["topk"], topk_host = topk_timing(T, zs, zt, turn, traj, mask, w, args.steps, args.warmup)
+    topk_host = None
+    if not in_place:
+        # further measurements on the same batch (the in-place batch's student
+        # logits now hold its gradient; those measurements exist out of place)
+        out["graph_replay"] = graph_timing(T, step, ws, args.steps)
+        out["depth_controller"] = depth_controller_timing(T, stats, w)
+        out["floor_and_outcome"] = options_timing(T, zs, zt, turn, traj, mask, w, grad,
+                                                  args.steps, args.warmup)
+        out["all_supervised"] = all_supervised_timing(T, zs, zt, turn, traj, w, grad, args.steps,
+                                                      args.warmup)
+        del grad
+        torch.cuda.empty_cache()
+        out["topk"], topk_host = topk_timing(T, zs, zt, turn, traj, mask, w, args.steps,
+                                             args.warmup)
     del zs, zt
     torch.cuda.empty_cache()
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(w, args.cpu_sample_tokens)
         out["cpu_baseline"]["depth_controller_update_us"] = oracle_controller_timing(stats_np, w)
-        out["cpu_baseline"]["topk_tokens_per_s"] = oracle_topk_timing(w, topk_host)
+        if topk_host is not None:
+            out["cpu_baseline"]["topk_tokens_per_s"] = oracle_topk_timing(w, topk_host)
     print(json.dumps(out), flush=True)
     return 0
 
