@@ -28,7 +28,8 @@
  * Conventions for every entry point:
  *   - Pointers are DEVICE pointers owned by the caller unless marked "host".
  *     The library allocates no memory and keeps no per-call state; all
- *     scratch lives in the caller's workspace.
+ *     scratch lives in the caller's workspace, except for
+ *     turnkl_fwd_bwd_noalloc, whose scratch is a fixed array in the library.
  *   - Measurement and test hooks are declared in turnkl_testing.h.
  *   - Work is enqueued on `stream` and is asynchronous; the success path never
  *     synchronises with the host.  Calls on distinct workspaces may run
@@ -69,6 +70,7 @@ typedef enum {
   TURNKL_ERR_SYNC_TIMEOUT = -8,  /* device: cross-workgroup exchange did not complete */
   TURNKL_ERR_TOPK_ID = -9,       /* device: a top-K support id outside [0, vocab) */
   TURNKL_ERR_OUTCOME = -10,      /* device: outcome flag not constant over a trajectory */
+  TURNKL_ERR_SCRATCH = -11,      /* turnkl_fwd_bwd_noalloc: problem larger than its scratch */
 } turnkl_status;
 
 /* Statistics of one turn index t over the supervised tokens at that turn. */
@@ -275,6 +277,41 @@ double turnkl_alpha_schedule(int64_t k, int64_t K, double s, double e);
 
 /* Static description of a return code.  Host function. */
 const char* turnkl_status_string(int status);
+
+/*
+ * turnkl_fwd_bwd without a workspace argument, for callers that cannot
+ * allocate device memory: code under HIP graph capture, tight serving loops,
+ * harnesses that forbid hipMalloc.  Arguments, results and errors are those
+ * of turnkl_fwd_bwd, except:
+ *   - The scratch is an array inside the library of
+ *     TURNKL_NOALLOC_SCRATCH_BYTES (32 MiB), one in the memory of every GPU
+ *     that runs the library, held until the process ends.  A problem whose
+ *     workspace would be larger (turnkl_workspace_bytes with aligned_rows = 1
+ *     when the rows are 16-byte aligned, else 0) returns TURNKL_ERR_SCRATCH
+ *     and enqueues nothing.  With aligned rows at vocab = 151,936 in bf16
+ *     that is above about 158,000 tokens (212 bytes per token).
+ *   - The call allocates nothing (no hipMalloc, hipFree or allocating library
+ *     routine).  Its first call on a device looks up the device address of
+ *     that device's array once.  `stream` must belong to the current device.
+ *   - status_out (device int32, 4-byte aligned, or NULL) receives TURNKL_OK
+ *     or the device-detected error when the call's last kernel runs: the role
+ *     turnkl_get_status plays for a workspace.
+ *   - All calls on one GPU share its array.  Calls ordered on one stream are
+ *     safe; calls that can overlap in time on one GPU (different streams or
+ *     host threads without ordering between them) race and give unspecified
+ *     results.  Every call initialises what it reads of the array.
+ */
+#define TURNKL_NOALLOC_SCRATCH_BYTES (32u << 20)
+
+int turnkl_fwd_bwd_noalloc(const void* student_logits, int64_t ld_student,
+                           const void* teacher_logits, int64_t ld_teacher, int dtype,
+                           int64_t n_tokens, int64_t vocab, const int32_t* turn_id,
+                           const int32_t* traj_id, const uint8_t* loss_mask, double alpha,
+                           float grad_scale, float* loss_out, void* grad_out, int64_t ld_grad,
+                           turnkl_turn_stat* turn_stats_out, int32_t max_turns,
+                           int accumulate_stats, float* token_kl_out,
+                           const turnkl_options* options, int32_t* status_out,
+                           hipStream_t stream);
 
 /* ------------------------------------------------------------------------
  * Top-K variant of the loss: the reverse KL on the teacher's top-K support

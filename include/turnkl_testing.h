@@ -17,8 +17,8 @@ extern "C" {
 #endif
 
 /*
- * Profiling hook: while both events are non-NULL, every turnkl_fwd_bwd call
- * made by this thread records `before`
+ * Profiling hook: while both events are non-NULL, every turnkl_fwd_bwd (and
+ * turnkl_fwd_bwd_noalloc) call made by this thread records `before`
  * immediately before and `after` immediately after its row kernel (the kernel
  * that reads the logits and writes the gradient), on the call's stream; a
  * turnkl_fwd_bwd_topk call brackets its support and dense-gradient kernels.

@@ -101,12 +101,14 @@ __global__ __launch_bounds__(kFinThreads) void finalize(Ws ws, int max_turns, fl
                                                        turnkl_turn_stat* stats,
                                                        turnkl_turn_stat* ostats,
                                                        const unsigned char* success,
-                                                       int accumulate) {
+                                                       int accumulate, int* status_out) {
   __shared__ Moments s_m[kFinThreads];
   __shared__ double s_l[3][kFinThreads];
-  const bool bad = ws.hdr->err_key != kNoError;
+  const unsigned long long key = ws.hdr->err_key;
+  const bool bad = key != kNoError;
   const int n_seg = ws.hdr->n_seg;
-  if ((int)blockIdx.x == 3 * max_turns) {  // the three losses
+  if ((int)blockIdx.x == 3 * max_turns) {  // the three losses (and the call's status)
+    if (status_out && threadIdx.x == 0) *status_out = status_from_key(key);
     if (bad) {
       if (threadIdx.x < 3) loss_out[threadIdx.x] = __builtin_nanf("");
       return;
@@ -177,7 +179,7 @@ __global__ __launch_bounds__(kFinThreads) void finalize(Ws ws, int max_turns, fl
 
 hipError_t launch_reduce(const SegParams& p, const Ws& ws, const float* kl, double alpha,
                          float* loss_out, turnkl_turn_stat* stats, turnkl_turn_stat* ostats,
-                         int accumulate, hipStream_t s) {
+                         int accumulate, int* status_out, hipStream_t s) {
   if (p.n > 0) {
     long long g = p.n < 4096 ? p.n : 4096;
     seg_moments<<<dim3((unsigned)g), dim3(kMomThreads), 0, s>>>(p, ws, kl, alpha);
@@ -185,7 +187,7 @@ hipError_t launch_reduce(const SegParams& p, const Ws& ws, const float* kl, doub
   }
   const int turns = (stats || ostats) ? p.max_turns : 0;
   finalize<<<dim3((unsigned)(3 * turns + 1)), dim3(kFinThreads), 0, s>>>(
-      ws, turns, loss_out, stats, ostats, p.success, accumulate);
+      ws, turns, loss_out, stats, ostats, p.success, accumulate, status_out);
   return hipGetLastError();
 }
 

@@ -6,6 +6,7 @@
 #include <string.h>
 
 #include <initializer_list>
+#include <mutex>
 
 #include "turnkl_internal.h"
 #include "turnkl_testing.h"
@@ -191,14 +192,43 @@ size_t workspace_bytes_for(int64_t n_tokens, int64_t vocab, int dtype, int32_t m
       .total;
 }
 
-// The fused call on a caller workspace.
+// ---------------------------------------------------------------------------
+// Scratch of the no-allocation entry point (turnkl_fwd_bwd_noalloc): one
+// array in every GPU's memory that runs the library, held until the process
+// ends.  Host code never passes the array's name to a kernel or a copy (on
+// the host it names a stand-in, not device memory): the device address comes
+// from hipGetSymbolAddress, taken once per device with that device current
+// and kept below.
+constexpr size_t kScratchBytes = TURNKL_NOALLOC_SCRATCH_BYTES;
+static __device__ __align__(256) unsigned char scratch[kScratchBytes];
+
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+void* g_scratch_ptr[kMaxDevices] = {};
+
+// The current device's address of `scratch`, or null when it cannot be had.
+void* scratch_address() {
+  int dev = -1;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDevices) return nullptr;
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (!g_scratch_ptr[dev]) {
+    void* ptr = nullptr;
+    if (hipGetSymbolAddress(&ptr, HIP_SYMBOL(scratch)) != hipSuccess || !ptr) return nullptr;
+    g_scratch_ptr[dev] = ptr;
+  }
+  return g_scratch_ptr[dev];
+}
+
+// The fused call on a given workspace.  noalloc: the workspace is the scratch
+// array (its own size check and error code); status_out: optional device
+// int32 that receives the device-side status at the end of the call.
 int fwd_bwd_impl(const void* student_logits, int64_t ld_student, const void* teacher_logits,
                  int64_t ld_teacher, int dtype, int64_t n_tokens, int64_t vocab,
                  const int32_t* turn_id, const int32_t* traj_id, const uint8_t* loss_mask,
                  double alpha, float grad_scale, float* loss_out, void* grad_out, int64_t ld_grad,
                  turnkl_turn_stat* turn_stats_out, int32_t max_turns, int accumulate_stats,
                  float* token_kl_out, const turnkl_options* options, void* workspace,
-                 size_t workspace_bytes, hipStream_t stream) {
+                 size_t workspace_bytes, bool noalloc, int32_t* status_out, hipStream_t stream) {
   // ---- arguments
   if (dtype != TURNKL_BF16 && dtype != TURNKL_F32) return TURNKL_ERR_INVALID_ARG;
   if (n_tokens < 0 || n_tokens > 0x7FFFFFFFll || vocab < 1 || max_turns < 1 ||
@@ -206,14 +236,15 @@ int fwd_bwd_impl(const void* student_logits, int64_t ld_student, const void* tea
     return TURNKL_ERR_INVALID_ARG;
   if (!(alpha >= 0.0 && alpha <= 1.0)) return TURNKL_ERR_INVALID_ARG;  // rejects NaN
   if (!isfinite(grad_scale)) return TURNKL_ERR_INVALID_ARG;
-  if (!loss_out || !workspace) return TURNKL_ERR_INVALID_ARG;
+  if (!loss_out || (!noalloc && !workspace)) return TURNKL_ERR_INVALID_ARG;
+  if (((uintptr_t)status_out & 3u) != 0) return TURNKL_ERR_INVALID_ARG;
   if (n_tokens > 0) {
     if (!student_logits || !teacher_logits || !turn_id || !traj_id || !loss_mask)
       return TURNKL_ERR_INVALID_ARG;
     if (ld_student < vocab || ld_teacher < vocab) return TURNKL_ERR_INVALID_ARG;
     if (grad_out && ld_grad < vocab) return TURNKL_ERR_INVALID_ARG;
   }
-  if (((uintptr_t)workspace & 255u) != 0) return TURNKL_ERR_WORKSPACE;
+  if (!noalloc && ((uintptr_t)workspace & 255u) != 0) return TURNKL_ERR_WORKSPACE;
 
   const size_t es = dtype == TURNKL_BF16 ? 2 : 4;
   const size_t ns = matrix_bytes(n_tokens, ld_student, vocab, es);
@@ -224,6 +255,12 @@ int fwd_bwd_impl(const void* student_logits, int64_t ld_student, const void* tea
     const bool in_place = grad_out == student_logits && ld_grad == ld_student;
     if (!in_place && overlaps(grad_out, ng, student_logits, ns)) return TURNKL_ERR_ALIAS;
   }
+  if (status_out &&
+      overlaps_any(status_out, 4, {{student_logits, ns}, {teacher_logits, nt}, {grad_out, ng},
+                                   {token_kl_out, (size_t)n_tokens * 4},
+                                   {loss_out, 3 * sizeof(float)},
+                                   {turn_stats_out, (size_t)max_turns * sizeof(turnkl_turn_stat)}}))
+    return TURNKL_ERR_ALIAS;
 
   // ---- row tiling: 16-byte vectors when every row start is 16-byte aligned
   RowTiling tiling = vector_tiling(vocab, dtype, t_vpt_override);
@@ -245,13 +282,20 @@ int fwd_bwd_impl(const void* student_logits, int64_t ld_student, const void* tea
   Extras ex;
   if (int rc = apply_options(options, n_tokens, max_turns, turn_stats_out,
                              {{student_logits, ns}, {teacher_logits, nt}, {grad_out, ng},
-                              {token_kl_out, (size_t)n_tokens * 4}, {loss_out, 3 * sizeof(float)}},
+                              {token_kl_out, (size_t)n_tokens * 4}, {loss_out, 3 * sizeof(float)},
+                              {status_out, status_out ? 4u : 0u}},
                              &sp, &ex))
     return rc;
 
   // the layout of this call: exchange slots for the path it takes
   const Layout L = make_layout(n_tokens, tiling.n_chunks > 1 ? tiling.n_chunks : 0, 0, max_turns);
-  if (workspace_bytes < L.total) return TURNKL_ERR_WORKSPACE;
+  if (noalloc) {
+    if (L.total > kScratchBytes) return TURNKL_ERR_SCRATCH;
+    workspace = scratch_address();
+    if (!workspace) return TURNKL_ERR_HIP;
+  } else if (workspace_bytes < L.total) {
+    return TURNKL_ERR_WORKSPACE;
+  }
   Ws ws = bind(workspace, L);
   if (ex.weights) ws.w = ex.weights;
   float* kl = token_kl_out ? token_kl_out : ws.kl;
@@ -286,7 +330,7 @@ int fwd_bwd_impl(const void* student_logits, int64_t ld_student, const void* tea
   if (prof && hipEventRecord(t_row_after, stream) != hipSuccess) return TURNKL_ERR_HIP;
 
   if (launch_reduce(sp, ws, kl, alpha, loss_out, turn_stats_out, ex.outcome_stats,
-                    accumulate_stats, stream) != hipSuccess)
+                    accumulate_stats, status_out, stream) != hipSuccess)
     return TURNKL_ERR_HIP;
   return TURNKL_OK;
 }
@@ -319,7 +363,22 @@ int turnkl_fwd_bwd(const void* student_logits, int64_t ld_student, const void* t
   return fwd_bwd_impl(student_logits, ld_student, teacher_logits, ld_teacher, dtype, n_tokens,
                       vocab, turn_id, traj_id, loss_mask, alpha, grad_scale, loss_out, grad_out,
                       ld_grad, turn_stats_out, max_turns, accumulate_stats, token_kl_out, options,
-                      workspace, workspace_bytes, stream);
+                      workspace, workspace_bytes, false, nullptr, stream);
+}
+
+int turnkl_fwd_bwd_noalloc(const void* student_logits, int64_t ld_student,
+                           const void* teacher_logits, int64_t ld_teacher, int dtype,
+                           int64_t n_tokens, int64_t vocab, const int32_t* turn_id,
+                           const int32_t* traj_id, const uint8_t* loss_mask, double alpha,
+                           float grad_scale, float* loss_out, void* grad_out, int64_t ld_grad,
+                           turnkl_turn_stat* turn_stats_out, int32_t max_turns,
+                           int accumulate_stats, float* token_kl_out,
+                           const turnkl_options* options, int32_t* status_out,
+                           hipStream_t stream) {
+  return fwd_bwd_impl(student_logits, ld_student, teacher_logits, ld_teacher, dtype, n_tokens,
+                      vocab, turn_id, traj_id, loss_mask, alpha, grad_scale, loss_out, grad_out,
+                      ld_grad, turn_stats_out, max_turns, accumulate_stats, token_kl_out, options,
+                      nullptr, 0, true, status_out, stream);
 }
 
 size_t turnkl_topk_workspace_bytes(int64_t n_tokens, int32_t k, int32_t max_turns) {
@@ -417,7 +476,7 @@ int turnkl_fwd_bwd_topk(const void* student_logits, int64_t ld_student, int dtyp
   if (launch_topk_dense(tp, stream) != hipSuccess) return TURNKL_ERR_HIP;
   if (prof && hipEventRecord(t_row_after, stream) != hipSuccess) return TURNKL_ERR_HIP;
   if (launch_reduce(sp, ws, kl, alpha, loss_out, turn_stats_out, ex.outcome_stats,
-                    accumulate_stats, stream) != hipSuccess)
+                    accumulate_stats, nullptr, stream) != hipSuccess)
     return TURNKL_ERR_HIP;
   return TURNKL_OK;
 }
@@ -477,6 +536,8 @@ const char* turnkl_status_string(int status) {
     case TURNKL_ERR_SYNC_TIMEOUT: return "row exchange timed out";
     case TURNKL_ERR_TOPK_ID: return "top-K support id outside [0, vocab)";
     case TURNKL_ERR_OUTCOME: return "outcome flag not constant over a trajectory";
+    case TURNKL_ERR_SCRATCH:
+      return "problem larger than the built-in scratch of turnkl_fwd_bwd_noalloc";
     default: return "unknown status";
   }
 }

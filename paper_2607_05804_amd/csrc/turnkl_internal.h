@@ -28,7 +28,7 @@ __host__ __device__ inline unsigned long long err_key(long long pos, unsigned pr
   return ((unsigned long long)pos << 4) | prio;
 }
 
-inline int status_from_key(unsigned long long key) {
+__host__ __device__ inline int status_from_key(unsigned long long key) {
   if (key == kNoError) return TURNKL_OK;
   switch ((unsigned)(key & 0xF)) {
     case kPrioPadMask: return TURNKL_ERR_PAD_MASK;
@@ -321,8 +321,10 @@ constexpr int kMaxTopK = 1024;
 hipError_t launch_topk_rows(const TopkParams& p, hipStream_t s);
 hipError_t launch_topk_dense(const TopkParams& p, hipStream_t s);
 
+// status_out: optional device int32 that receives the call's status
+// (TURNKL_OK or the device-detected error) once the loss is written.
 hipError_t launch_reduce(const SegParams& p, const Ws& ws, const float* kl, double alpha,
                          float* loss_out, turnkl_turn_stat* stats, turnkl_turn_stat* ostats,
-                         int accumulate, hipStream_t s);
+                         int accumulate, int* status_out, hipStream_t s);
 
 }  // namespace turnkl

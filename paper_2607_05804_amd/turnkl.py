@@ -28,12 +28,17 @@ ERR_HIP = -7
 ERR_SYNC_TIMEOUT = -8
 ERR_TOPK_ID = -9
 ERR_OUTCOME = -10
+ERR_SCRATCH = -11
+
+# Size of the scratch array of turnkl_fwd_bwd_noalloc (TURNKL_NOALLOC_SCRATCH_BYTES).
+NOALLOC_SCRATCH_BYTES = 32 << 20
 
 BF16 = 0
 F32 = 1
 
 # Names of every entry point include/turnkl.h declares.
-EXPORTS = ("turnkl_workspace_bytes", "turnkl_fwd_bwd", "turnkl_get_status", "turnkl_get_segments", "turnkl_alpha_schedule",
+EXPORTS = ("turnkl_workspace_bytes", "turnkl_fwd_bwd", "turnkl_fwd_bwd_noalloc",
+           "turnkl_get_status", "turnkl_get_segments", "turnkl_alpha_schedule",
            "turnkl_status_string", "turnkl_topk_workspace_bytes", "turnkl_fwd_bwd_topk",
            "turnkl_depth_default_config", "turnkl_depth_init", "turnkl_depth_plan",
            "turnkl_depth_update", "turnkl_loss_share", "turnkl_budget_report",
@@ -110,6 +115,12 @@ def lib() -> ctypes.CDLL:
             c.c_void_p, c.c_void_p, c.c_void_p, c.c_double, c.c_float, c.c_void_p, c.c_void_p,
             c.c_int64, c.c_void_p, c.c_int32, c.c_int, c.c_void_p, c.POINTER(Options),
             c.c_void_p, c.c_size_t, c.c_void_p]
+        l.turnkl_fwd_bwd_noalloc.restype = c.c_int
+        l.turnkl_fwd_bwd_noalloc.argtypes = [
+            c.c_void_p, c.c_int64, c.c_void_p, c.c_int64, c.c_int, c.c_int64, c.c_int64,
+            c.c_void_p, c.c_void_p, c.c_void_p, c.c_double, c.c_float, c.c_void_p, c.c_void_p,
+            c.c_int64, c.c_void_p, c.c_int32, c.c_int, c.c_void_p, c.POINTER(Options),
+            c.c_void_p, c.c_void_p]
         l.turnkl_get_status.restype = c.c_int
         l.turnkl_get_status.argtypes = [c.c_void_p, c.c_void_p]
         l.turnkl_get_segments.restype = c.c_int
@@ -328,7 +339,7 @@ def _check_fused_inputs(student, teacher, turn_id, traj_id, loss_mask):
 
 def _fused_args(student, teacher, dt, n, v, turn_id, traj_id, loss_mask, alpha, grad_scale,
                 loss, grad_t, turn_stats, max_turns, accumulate_stats, kl_t, options):
-    """turnkl_fwd_bwd's arguments before the workspace, in order."""
+    """The arguments turnkl_fwd_bwd and turnkl_fwd_bwd_noalloc share, in order."""
     return [_ptr(student), _row_stride(student) if n else v, _ptr(teacher),
             _row_stride(teacher) if n else v, dt, n, v, _ptr(turn_id), _ptr(traj_id),
             _ptr(loss_mask), float(alpha), float(grad_scale), _ptr(loss), _ptr(grad_t),
@@ -395,6 +406,47 @@ def fwd_bwd(student: torch.Tensor, teacher: torch.Tensor, turn_id: torch.Tensor,
         if st != OK:
             raise TurnKLError(st, "turnkl_fwd_bwd (device)")
     return loss, grad_t, turn_stats, kl_t, workspace
+
+
+def fwd_bwd_noalloc(student: torch.Tensor, teacher: torch.Tensor, turn_id: torch.Tensor,
+                    traj_id: torch.Tensor, loss_mask: torch.Tensor, alpha: float,
+                    loss: torch.Tensor, *, grad_scale: float = 1.0,
+                    grad: str | torch.Tensor | None = None, max_turns: int = 64,
+                    turn_stats: torch.Tensor | None = None, accumulate_stats: bool = False,
+                    token_kl: torch.Tensor | None = None, status: torch.Tensor | None = None,
+                    support_floor: int = 0, support_frac: float = 0.0,
+                    success: torch.Tensor | None = None,
+                    outcome_stats: torch.Tensor | None = None,
+                    token_weights: torch.Tensor | None = None,
+                    token_lse: torch.Tensor | None = None) -> None:
+    """turnkl_fwd_bwd_noalloc on the current stream: the fused call with the
+    library's built-in scratch instead of a workspace.  Neither the library
+    nor this function allocates: every output is the caller's tensor.
+
+    loss: float32 [3]; grad: a tensor, "inplace" or None (forward only);
+    token_kl: float32 [N] or None; status: int32 [1] or None, receives the
+    device-side status (OK or the data error) when the call's last kernel
+    runs.  The other arguments are those of fwd_bwd.  Calls that can overlap
+    in time on one GPU share the scratch and race.
+    """
+    dt, n, v = _check_fused_inputs(student, teacher, turn_id, traj_id, loss_mask)
+    dev = student.device
+    grad_t = student if (isinstance(grad, str) and grad == "inplace") else grad
+    if isinstance(grad_t, str):
+        raise ValueError(grad)
+    _need(loss, 12, "loss", dev, torch.float32)
+    _need(status, 4, "status", dev, torch.int32)
+    _check_common(student, n, max_turns, turn_id, traj_id, loss_mask, turn_stats, outcome_stats,
+                  token_kl, grad_t)
+    stream = torch.cuda.current_stream(dev).cuda_stream
+    opts = _options(n, support_floor, support_frac, success, outcome_stats, token_weights,
+                    token_lse, dev)
+    rc = lib().turnkl_fwd_bwd_noalloc(
+        *_fused_args(student, teacher, dt, n, v, turn_id, traj_id, loss_mask, alpha, grad_scale,
+                     loss, grad_t, turn_stats, max_turns, accumulate_stats, token_kl, opts),
+        _ptr(status), ctypes.c_void_p(stream))
+    if rc != OK:
+        raise TurnKLError(rc, "turnkl_fwd_bwd_noalloc")
 
 
 class TopkWorkspace(Workspace):

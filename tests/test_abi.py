@@ -33,7 +33,7 @@ def test_every_declared_symbol_is_exported():
 
 def test_status_strings_and_alpha_schedule():
     assert T.status_string(T.OK) == "ok"
-    for code in range(-10, 0):
+    for code in range(-11, 0):
         assert T.status_string(code) != "unknown status"
     assert T.status_string(-99) == "unknown status"
     assert T.alpha_schedule(0, 100) == 0.0
@@ -74,6 +74,8 @@ def test_workspace_bytes_sized_for_the_path_the_call_takes():
         T.set_row_tiling(0)
     assert int(lib.turnkl_testing_workspace_bytes(n, v, T.BF16, 50, 1, 0)) == aligned
     assert int(lib.turnkl_testing_workspace_bytes(n, v, T.BF16, 50, 1, 26)) == 0
+    # the stress batch fits the no-allocation entry point's scratch
+    assert _ws(131072, v, T.BF16, 200, 1) <= T.NOALLOC_SCRATCH_BYTES
 
 
 def test_workspace_bytes():
@@ -216,6 +218,43 @@ def test_unaligned_rows_run_with_a_workspace_sized_for_them():
     assert _call(aligned=False, **kw) not in (T.ERR_WORKSPACE, T.ERR_INVALID_ARG, T.ERR_ALIAS)
 
 
+def _call_noalloc(**kw):
+    """turnkl_fwd_bwd_noalloc with fake (never dereferenced) addresses."""
+    n, v = kw.get("n", 64), kw.get("v", 1024)
+    args = dict(zs=0x100000000, ld_s=v, zt=0x200000000, ld_t=v, dtype=T.BF16, n=n, v=v,
+                turn=0x300000000, traj=0x300100000, mask=0x300200000, alpha=0.5, scale=1.0,
+                loss=0x300300000, grad=0x400000000, ld_g=v, stats=0, max_turns=8, acc=0, kl=0,
+                opts=None, status=0x300400000)
+    args.update(kw)
+    p = lambda x: ctypes.c_void_p(x) if x else None
+    return T.lib().turnkl_fwd_bwd_noalloc(
+        p(args["zs"]), args["ld_s"], p(args["zt"]), args["ld_t"], args["dtype"], args["n"],
+        args["v"], p(args["turn"]), p(args["traj"]), p(args["mask"]), args["alpha"],
+        args["scale"], p(args["loss"]), p(args["grad"]), args["ld_g"], p(args["stats"]),
+        args["max_turns"], args["acc"], p(args["kl"]), _opts(args["opts"]), p(args["status"]),
+        None)
+
+
+@pytest.mark.parametrize("kw,code", [
+    (dict(alpha=2.0), T.ERR_INVALID_ARG),
+    (dict(loss=0), T.ERR_INVALID_ARG),
+    (dict(zs=0), T.ERR_INVALID_ARG),
+    (dict(grad=0x200000000), T.ERR_ALIAS),
+    (dict(status=0x300400002), T.ERR_INVALID_ARG),  # status_out not 4-byte aligned
+    (dict(status=0x300300004), T.ERR_ALIAS),        # inside loss_out
+    (dict(status=0x100000000 + 64), T.ERR_ALIAS),   # inside the student logits
+    (dict(opts=(-1, 0.0, 0, 0)), T.ERR_INVALID_ARG),
+    # larger than the 32 MiB scratch: 212 bytes per token at V = 151,936 with
+    # aligned rows, 724 on the element-wise path
+    (dict(n=160000, v=151936, ld_s=151936, ld_t=151936, ld_g=151936, zs=0x1000000000,
+          zt=0x3000000000, grad=0x5000000000), T.ERR_SCRATCH),
+    (dict(n=50000, v=151936, ld_s=151937, ld_t=151937, ld_g=151937, zs=0x1000000000,
+          zt=0x3000000000, grad=0x5000000000), T.ERR_SCRATCH),
+])
+def test_noalloc_host_rejects_before_launch(kw, code):
+    assert _call_noalloc(**kw) == code
+
+
 def test_binding_fails_loudly_without_library(monkeypatch, tmp_path):
     monkeypatch.setattr(T, "_lib", None)
     monkeypatch.setattr(T, "LIB_PATH", str(tmp_path / "missing.so"))
@@ -299,6 +338,7 @@ def test_header_is_plain_c_and_links(tmp_path):
 int main(void) {
   size_t b = turnkl_workspace_bytes(1000, 151936, TURNKL_BF16, 50, 1);
   if (turnkl_testing_workspace_bytes(1000, 151936, TURNKL_BF16, 50, 1, 0) != b) return 3;
+  if (TURNKL_NOALLOC_SCRATCH_BYTES < b) return 4;
   turnkl_depth_config c;
   turnkl_depth_default_config(&c);
   if (b == 0 || c.h_max < c.h_min) return 1;
