@@ -6,15 +6,20 @@
 //   KL_i = sum_{v in S_i} p^_s(v) d_v,  d_v = log p^_s(v) - log p^_t(v),
 //   dKL_i/da_v = p^_s(v) (d_v - KL_i) on S_i, 0 elsewhere.
 //
-// topk_rows   one wave per token: gathers the K student logits at the
+// topk_rows   one wave per token (four tokens per wave for K <= 64, their
+//             loads issued together): gathers the K student logits at the
 //             support ids (one scattered load per id), reduces max and sum
 //             of both distributions with wave shuffles, writes KL_i and
-//             grad_scale * w_i * dKL_i/da on the support to the stage.
+//             grad_scale * w_i * dKL_i/da on the support to the stage (the
+//             caller's sparse output, or the workspace);
 // topk_fill   zero-fills the vocab columns of every dense gradient row with
 //             16-byte streaming stores;
-// topk_scatter  then writes the staged support values of each supervised
-//             row (one wave per row).  All reads of the student logits happen
-//             in topk_rows, so a dense gradient may overwrite them (in place).
+// topk_scatter  writes the staged support values of each supervised row.
+//
+// Order.  An out-of-place dense gradient is zero-filled first, and topk_rows
+// then writes the support values into it directly (no scatter kernel, no
+// staging round trip).  In place, topk_rows reads every student logit and
+// stages the values, then the fill and the scatter overwrite the rows.
 
 #include <hip/hip_bf16.h>
 
@@ -41,81 +46,114 @@ __device__ inline float load_logit(const void* base, long long i, bool bf16) {
 
 __device__ inline float wave_max_f(float v) { return wave_max(v); }
 
-// kPer support entries per lane (K <= 64 kPer).
-template <int kPer>
+// kPer support entries per lane (K <= 64 kPer); kRows rows per wave, their
+// loads issued together (the kernel is bound by the latency of the id loads
+// and the gathers that depend on them).  The scaled gradient on the support
+// goes to the stage (when there is one) and, with p.direct, straight into a
+// zero-filled, out-of-place dense gradient.
+template <int kPer, int kRows>
 __global__ __launch_bounds__(kThreads) void topk_rows(TopkParams p) {
   if (p.hdr->err_key != kNoError) return;
   const int lane = threadIdx.x & (kWave - 1);
   const long long wave0 = (long long)blockIdx.x * kWavesPerBlock + threadIdx.x / kWave;
   const long long stride = (long long)gridDim.x * kWavesPerBlock;
-  for (long long row = wave0; row < p.n_rows; row += stride) {
-    float* stage = p.stage + row * p.ld_stage;
-    if (!p.mask[row]) {
-      if (p.zero_masked_stage)
-        for (int j = lane; j < p.k; j += kWave) stage[j] = 0.0f;
-      if (p.lse && lane == 0) {  // the row is not read: no log-partition function
-        p.lse[2 * row] = __builtin_nanf("");
-        p.lse[2 * row + 1] = __builtin_nanf("");
+  for (long long r0 = wave0 * kRows; r0 < p.n_rows; r0 += stride * kRows) {
+    bool sup[kRows], bad[kRows], on[kRows][kPer];
+    int id[kRows][kPer];
+    float a[kRows][kPer], b[kRows][kPer];
+    // every load of the kRows rows first: masks, ids and teacher values ...
+#pragma unroll
+    for (int r = 0; r < kRows; ++r) {
+      const long long row = r0 + r;
+      sup[r] = row < p.n_rows && p.mask[row];
+      bad[r] = false;
+#pragma unroll
+      for (int q = 0; q < kPer; ++q) {
+        const int j = lane + q * kWave;
+        on[r][q] = sup[r] && j < p.k;
+        id[r][q] = on[r][q] ? p.ids[row * p.ld_k + j] : 0;
+        b[r][q] = on[r][q] ? p.vals[row * p.ld_k + j] : -INFINITY;
       }
-      continue;
     }
-    float a[kPer], b[kPer];
-    bool on[kPer];
-    bool bad = false;
+    // ... then the student logits at the support ids
 #pragma unroll
-    for (int q = 0; q < kPer; ++q) {
-      const int j = lane + q * kWave;
-      on[q] = j < p.k;
-      const int id = on[q] ? p.ids[row * p.ld_k + j] : 0;
-      const bool in = id >= 0 && id < p.vocab;
-      bad = bad || (on[q] && !in);
-      on[q] = on[q] && in;
-      b[q] = on[q] ? p.vals[row * p.ld_k + j] : -INFINITY;
-      a[q] = on[q] ? load_logit(p.zs, row * p.ld_s + id, p.bf16) : -INFINITY;
-    }
-    if (__ballot(bad) != 0ull) {
-      if (lane == 0) atomicMin(&p.hdr->err_key, err_key(row, kPrioTopkId));
-      continue;
-    }
-    float ma = -INFINITY, mb = -INFINITY;
+    for (int r = 0; r < kRows; ++r) {
 #pragma unroll
-    for (int q = 0; q < kPer; ++q) {
-      ma = fmaxf(ma, a[q]);
-      mb = fmaxf(mb, b[q]);
+      for (int q = 0; q < kPer; ++q) {
+        const bool in = id[r][q] >= 0 && id[r][q] < p.vocab;
+        bad[r] = bad[r] || (on[r][q] && !in);
+        on[r][q] = on[r][q] && in;
+        a[r][q] = on[r][q] ? load_logit(p.zs, (r0 + r) * p.ld_s + id[r][q], p.bf16) : -INFINITY;
+        b[r][q] = on[r][q] ? b[r][q] : -INFINITY;
+      }
     }
-    ma = wave_max_f(ma);
-    mb = wave_max_f(mb);
-    float sa = 0.0f, sb = 0.0f;
 #pragma unroll
-    for (int q = 0; q < kPer; ++q) {
-      sa += on[q] ? expf(a[q] - ma) : 0.0f;
-      sb += on[q] ? expf(b[q] - mb) : 0.0f;
-    }
-    sa = wave_sum(sa);
-    sb = wave_sum(sb);
-    const float la = logf(sa);
-    const float lb = logf(sb);
-    float d[kPer], pr[kPer];
-    float kl = 0.0f;
+    for (int r = 0; r < kRows; ++r) {
+      const long long row = r0 + r;
+      if (row >= p.n_rows) break;
+      float* stage = p.stage ? p.stage + row * p.ld_stage : nullptr;
+      if (!sup[r]) {
+        if (stage && p.zero_masked_stage)
+          for (int j = lane; j < p.k; j += kWave) stage[j] = 0.0f;
+        if (p.lse && lane == 0) {  // the row is not read: no log-partition function
+          p.lse[2 * row] = __builtin_nanf("");
+          p.lse[2 * row + 1] = __builtin_nanf("");
+        }
+        continue;
+      }
+      if (__ballot(bad[r]) != 0ull) {
+        if (lane == 0) atomicMin(&p.hdr->err_key, err_key(row, kPrioTopkId));
+        continue;
+      }
+      float ma = -INFINITY, mb = -INFINITY;
 #pragma unroll
-    for (int q = 0; q < kPer; ++q) {
-      const float xa = a[q] - ma;
-      d[q] = on[q] ? ((xa - (b[q] - mb)) - (la - lb)) : 0.0f;
-      pr[q] = on[q] ? expf(xa - la) : 0.0f;
-      kl = fmaf(pr[q], d[q], kl);
-    }
-    kl = wave_sum(kl);
-    const float sc = p.wsc[row];
+      for (int q = 0; q < kPer; ++q) {
+        ma = fmaxf(ma, a[r][q]);
+        mb = fmaxf(mb, b[r][q]);
+      }
+      ma = wave_max_f(ma);
+      mb = wave_max_f(mb);
+      float sa = 0.0f, sb = 0.0f;
 #pragma unroll
-    for (int q = 0; q < kPer; ++q) {
-      const int j = lane + q * kWave;
-      if (j < p.k) stage[j] = sc * (pr[q] * (d[q] - kl));
-    }
-    if (lane == 0) {
-      p.kl[row] = kl;
-      if (p.lse) {  // log sum exp over the support = max + ln(sum)
-        p.lse[2 * row] = ma + la;
-        p.lse[2 * row + 1] = mb + lb;
+      for (int q = 0; q < kPer; ++q) {
+        sa += on[r][q] ? expf(a[r][q] - ma) : 0.0f;
+        sb += on[r][q] ? expf(b[r][q] - mb) : 0.0f;
+      }
+      sa = wave_sum(sa);
+      sb = wave_sum(sb);
+      const float la = logf(sa);
+      const float lb = logf(sb);
+      float d[kPer], pr[kPer];
+      float kl = 0.0f;
+#pragma unroll
+      for (int q = 0; q < kPer; ++q) {
+        const float xa = a[r][q] - ma;
+        d[q] = on[r][q] ? ((xa - (b[r][q] - mb)) - (la - lb)) : 0.0f;
+        pr[q] = on[r][q] ? expf(xa - la) : 0.0f;
+        kl = fmaf(pr[q], d[q], kl);
+      }
+      kl = wave_sum(kl);
+      const float sc = p.wsc[row];
+#pragma unroll
+      for (int q = 0; q < kPer; ++q) {
+        const int j = lane + q * kWave;
+        if (j >= p.k) continue;
+        const float g = sc * (pr[q] * (d[q] - kl));
+        if (stage) stage[j] = g;
+        if (p.direct && on[r][q]) {
+          if (p.bf16) {
+            reinterpret_cast<__hip_bfloat16*>(p.grad)[row * p.ld_g + id[r][q]] = __float2bfloat16(g);
+          } else {
+            reinterpret_cast<float*>(p.grad)[row * p.ld_g + id[r][q]] = g;
+          }
+        }
+      }
+      if (lane == 0) {
+        p.kl[row] = kl;
+        if (p.lse) {  // log sum exp over the support = max + ln(sum)
+          p.lse[2 * row] = ma + la;
+          p.lse[2 * row + 1] = mb + lb;
+        }
       }
     }
   }
@@ -164,24 +202,34 @@ __global__ __launch_bounds__(kThreads) void topk_fill_flat(TopkParams p, long lo
 }
 
 // Scatter of the staged support values into the zero-filled rows of
-// supervised tokens, one wave per row; runs after topk_fill on the stream.
-template <bool kBf16>
+// supervised tokens (in place: the rows were read before the fill), kRows
+// rows per wave with their loads issued together; runs after topk_fill on
+// the stream.
+template <bool kBf16, int kRows>
 __global__ __launch_bounds__(kThreads) void topk_scatter(TopkParams p) {
   if (p.hdr->err_key != kNoError) return;
   const int lane = threadIdx.x & (kWave - 1);
   const long long wave0 = (long long)blockIdx.x * kWavesPerBlock + threadIdx.x / kWave;
   const long long stride = (long long)gridDim.x * kWavesPerBlock;
-  for (long long row = wave0; row < p.n_rows; row += stride) {
-    if (!p.mask[row]) continue;
-    const float* stage = p.stage + row * p.ld_stage;
-    for (int j = lane; j < p.k; j += kWave) {
-      const int id = p.ids[row * p.ld_k + j];
-      if (id < 0 || id >= p.vocab) continue;  // reported by topk_rows
-      const float x = stage[j];
-      if (kBf16) {
-        reinterpret_cast<__hip_bfloat16*>(p.grad)[row * p.ld_g + id] = __float2bfloat16(x);
-      } else {
-        reinterpret_cast<float*>(p.grad)[row * p.ld_g + id] = x;
+  for (long long r0 = wave0 * kRows; r0 < p.n_rows; r0 += stride * kRows) {
+    for (int j0 = 0; j0 < p.k; j0 += kWave) {
+      const int j = j0 + lane;
+      bool on[kRows];
+      int id[kRows];
+      float x[kRows];
+#pragma unroll
+      for (int r = 0; r < kRows; ++r) {
+        const long long row = r0 + r;
+        on[r] = row < p.n_rows && j < p.k && p.mask[row];
+        id[r] = on[r] ? p.ids[row * p.ld_k + j] : 0;
+        x[r] = on[r] ? p.stage[row * p.ld_stage + j] : 0.0f;
+      }
+#pragma unroll
+      for (int r = 0; r < kRows; ++r) {
+        if (!on[r] || id[r] < 0 || id[r] >= p.vocab) continue;  // bad ids: reported by topk_rows
+        const long long at = (r0 + r) * p.ld_g + id[r];
+        if (kBf16) reinterpret_cast<__hip_bfloat16*>(p.grad)[at] = __float2bfloat16(x[r]);
+        else reinterpret_cast<float*>(p.grad)[at] = x[r];
       }
     }
   }
@@ -207,12 +255,18 @@ void launch_fill_rows(const TopkParams& p, bool vec, hipStream_t s) {
 
 }  // namespace
 
+// Rows per wave of topk_rows and topk_scatter: four for a support of at
+// most 64 ids (one per lane), two up to 128, one beyond.
+constexpr int rows_per_wave(int per) { return per <= 1 ? 4 : per <= 2 ? 2 : 1; }
+
 hipError_t launch_topk_rows(const TopkParams& p, hipStream_t s) {
   if (p.n_rows == 0) return hipSuccess;
-  const int grid = grid_for(p.n_rows, kWavesPerBlock, 16384);
   const int per = (p.k + kWave - 1) / kWave;
-#define TURNKL_TOPK(n) \
-  case n: topk_rows<n><<<grid, kThreads, 0, s>>>(p); break;
+#define TURNKL_TOPK(n)                                                                     \
+  case n:                                                                                  \
+    topk_rows<n, rows_per_wave(n)>                                                         \
+        <<<grid_for(p.n_rows, kWavesPerBlock * rows_per_wave(n), 16384), kThreads, 0, s>>>(p); \
+    break;
   switch (per <= 1 ? 1 : per <= 2 ? 2 : per <= 4 ? 4 : per <= 8 ? 8 : 16) {
     TURNKL_TOPK(1) TURNKL_TOPK(2) TURNKL_TOPK(4) TURNKL_TOPK(8) TURNKL_TOPK(16)
     default: return hipErrorInvalidValue;
@@ -221,7 +275,7 @@ hipError_t launch_topk_rows(const TopkParams& p, hipStream_t s) {
   return hipGetLastError();
 }
 
-hipError_t launch_topk_dense(const TopkParams& p, hipStream_t s) {
+hipError_t launch_topk_fill(const TopkParams& p, hipStream_t s) {
   if (p.n_rows == 0 || !p.grad) return hipSuccess;
   const int es = p.bf16 ? 2 : 4;
   const bool vec = ((uintptr_t)p.grad % 16 == 0) && (p.ld_g * es) % 16 == 0 && (p.vocab * es) % 16 == 0;
@@ -231,10 +285,15 @@ hipError_t launch_topk_dense(const TopkParams& p, hipStream_t s) {
   } else {
     launch_fill_rows(p, vec, s);
   }
-  if (hipError_t e = hipGetLastError(); e != hipSuccess) return e;
-  const int grid = grid_for(p.n_rows, kWavesPerBlock, 16384);
-  if (p.bf16) topk_scatter<true><<<grid, kThreads, 0, s>>>(p);
-  else topk_scatter<false><<<grid, kThreads, 0, s>>>(p);
+  return hipGetLastError();
+}
+
+hipError_t launch_topk_scatter(const TopkParams& p, hipStream_t s) {
+  if (p.n_rows == 0 || !p.grad) return hipSuccess;
+  constexpr int kRows = 4;
+  const int grid = grid_for(p.n_rows, kWavesPerBlock * kRows, 16384);
+  if (p.bf16) topk_scatter<true, kRows><<<grid, kThreads, 0, s>>>(p);
+  else topk_scatter<false, kRows><<<grid, kThreads, 0, s>>>(p);
   return hipGetLastError();
 }
 

@@ -470,10 +470,20 @@ int turnkl_fwd_bwd_topk(const void* student_logits, int64_t ld_student, int dtyp
   tp.bf16 = dtype == TURNKL_BF16;
   tp.zero_masked_stage = grad_topk_out != nullptr;
   tp.lse = ex.lse;
+  // out of place: fill the dense gradient first, then the rows write their
+  // support values into it; in place the rows must read the logits first
+  tp.direct = grad_out != nullptr && grad_out != student_logits;
+  if (tp.direct) tp.stage = grad_topk_out;
   const bool prof = t_row_before && t_row_after;
   if (prof && hipEventRecord(t_row_before, stream) != hipSuccess) return TURNKL_ERR_HIP;
-  if (launch_topk_rows(tp, stream) != hipSuccess) return TURNKL_ERR_HIP;
-  if (launch_topk_dense(tp, stream) != hipSuccess) return TURNKL_ERR_HIP;
+  if (tp.direct) {
+    if (launch_topk_fill(tp, stream) != hipSuccess) return TURNKL_ERR_HIP;
+    if (launch_topk_rows(tp, stream) != hipSuccess) return TURNKL_ERR_HIP;
+  } else {
+    if (launch_topk_rows(tp, stream) != hipSuccess) return TURNKL_ERR_HIP;
+    if (launch_topk_fill(tp, stream) != hipSuccess) return TURNKL_ERR_HIP;
+    if (launch_topk_scatter(tp, stream) != hipSuccess) return TURNKL_ERR_HIP;
+  }
   if (prof && hipEventRecord(t_row_after, stream) != hipSuccess) return TURNKL_ERR_HIP;
   if (launch_reduce(sp, ws, kl, alpha, loss_out, turn_stats_out, ex.outcome_stats,
                     accumulate_stats, nullptr, stream) != hipSuccess)

@@ -314,12 +314,15 @@ struct TopkParams {
   int bf16;
   int zero_masked_stage;  // write zeros to stage rows of unsupervised tokens
   float* lse;             // [n_rows][2] log-partition functions on the support, or null
+  int direct;             // topk_rows also writes the support values into grad
+                          // (out of place, after the fill); stage may then be null
 };
 
 constexpr int kMaxTopK = 1024;
 
 hipError_t launch_topk_rows(const TopkParams& p, hipStream_t s);
-hipError_t launch_topk_dense(const TopkParams& p, hipStream_t s);
+hipError_t launch_topk_fill(const TopkParams& p, hipStream_t s);
+hipError_t launch_topk_scatter(const TopkParams& p, hipStream_t s);
 
 // status_out: optional device int32 that receives the call's status
 // (TURNKL_OK or the device-detected error) once the loss is written.

@@ -82,17 +82,41 @@ _NOT_VGPR_WRITERS = ("v_cmp", "v_readfirstlane", "v_readlane", "s_")
 
 def store_data_hazards(asm: str, window: int = WINDOW):
     """Wide stores whose data registers an instruction rewrites within
-    `window` instructions with no full vector-memory drain in between:
-    [(function, store, offending instruction, distance)]."""
-    instrs, fn = [], None
+    `window` executed instructions after the store, with no full
+    vector-memory drain in between: [(function, store, offending instruction,
+    distance)].  The scan follows the code as it runs on the fall-through
+    path: an unconditional branch continues at its target, a conditional one
+    falls through (its other side is often unreachable from the store, being
+    decided by a value set on the store's own path)."""
+    instrs, labels, fn = [], {}, None
     for line in asm.splitlines():
         m = re.match(r"^([A-Za-z_]\w*):", line)
         if m:
             fn = m.group(1)
+        m = re.match(r"^(\.L\w+):", line)
+        if m:
+            labels[m.group(1)] = len(instrs)
+            continue
         s = line.split(";")[0].strip()
         if not s or s.endswith(":") or s.startswith("."):
             continue
         instrs.append((fn, s))
+
+    def successors(i):
+        op = instrs[i][1].split()
+        if op[0] in ("s_endpgm", "s_setpc_b64", "s_trap"):
+            return []
+        if op[0] == "s_branch":
+            return [labels[op[1]]] if op[1] in labels else []
+        return [i + 1]
+
+    def writes(s2, data):
+        op = s2.split()[0]
+        if not op.startswith(_WRITERS) or op.startswith(_NOT_VGPR_WRITERS) or op.startswith("v_cmpx"):
+            return False
+        parts = s2.split()
+        return len(parts) > 1 and bool(_regs(parts[1].rstrip(",")) & data)
+
     found = []
     for i, (f, s) in enumerate(instrs):
         if not _WIDE_STORE.match(s):
@@ -100,23 +124,21 @@ def store_data_hazards(asm: str, window: int = WINDOW):
         ops = [t.rstrip(",") for t in s.split()[1:]]
         # global/flat/scratch: vaddr, vdata, ...; buffer: vdata, vaddr, ...
         data = _regs(ops[0] if s.startswith("buffer") else ops[1])
-        for k in range(1, window + 1):
-            if i + k >= len(instrs) or instrs[i + k][0] != f:
-                break
-            s2 = instrs[i + k][1]
-            op = s2.split()[0]
-            if op == "s_waitcnt" and "vmcnt(0)" in s2:
-                break
-            if op.startswith("s_endpgm"):
-                break
-            if not op.startswith(_WRITERS) or op.startswith(_NOT_VGPR_WRITERS):
+        seen, todo, hit = set(), [(j, 1) for j in successors(i)], None
+        while todo and hit is None:
+            j, k = todo.pop()
+            if k > window or j >= len(instrs) or instrs[j][0] != f or (j, k) in seen:
                 continue
-            if op.startswith("v_cmpx"):
+            seen.add((j, k))
+            s2 = instrs[j][1]
+            if s2.split()[0] == "s_waitcnt" and "vmcnt(0)" in s2:
                 continue
-            parts = s2.split()
-            if len(parts) > 1 and _regs(parts[1].rstrip(",")) & data:
-                found.append((f, s, s2, k))
+            if writes(s2, data):
+                hit = (f, s, s2, k)
                 break
+            todo += [(n, k + 1) for n in successors(j)]
+        if hit:
+            found.append(hit)
     return found
 
 
@@ -134,6 +156,13 @@ def test_scanner_catches_a_planted_hazard():
     assert not store_data_hazards(base + "  v_cmp_gt_f32_e32 vcc, v5, v6\n")
     far = "".join(f"  v_mov_b32_e32 v{20 + j}, 0\n" for j in range(WINDOW))
     assert not store_data_hazards(base + far + "  v_mov_b32_e32 v5, 0\n")
+    # control flow: the scan continues at an unconditional branch's target
+    assert not store_data_hazards(base + "  s_branch .LBB0_2\n  v_mov_b32_e32 v5, 0\n"
+                                  ".LBB0_2:\n  s_waitcnt vmcnt(0)\n  v_mov_b32_e32 v5, 1\n")
+    assert store_data_hazards(base + "  s_branch .LBB0_3\n  s_waitcnt vmcnt(0)\n"
+                              ".LBB0_3:\n  v_mov_b32_e32 v6, 1\n")
+    assert store_data_hazards(base + "  s_cbranch_scc1 .LBB0_4\n  v_mov_b32_e32 v7, 1\n"
+                              ".LBB0_4:\n  s_waitcnt vmcnt(0)\n")
 
 
 def test_row_kernel_fits_256_vgprs_without_spills(device_asm):

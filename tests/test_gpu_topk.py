@@ -90,6 +90,38 @@ def test_topk_parity(V, dtype, k, gpu):
     check_topk_grads(gk, g, ref, ids, 1.0, rows, mask, dtype == "bf16")
 
 
+@pytest.mark.parametrize("dtype,V,grad", [("bf16", 1792, "new"), ("bf16", 1792, "inplace"),
+                                          ("f32", 896, "new")])
+def test_topk_support_at_row_ends(dtype, V, grad, gpu):
+    """Support ids at the ends of rows of 224 16-byte packs, so that the
+    dense writes of neighbouring rows meet inside one 1 KiB span of the flat
+    gradient: both rows' edge packs hold support values, only the first's,
+    only the second's, or neither, next to masked rows too.  Every element
+    of the dense gradient is compared."""
+    log(f"topk support at row ends {dtype} V={V} {grad}")
+    traj, turn, mask, zs_h, zt_h = make_batch(97, V=V, dtype=dtype)
+    n, k = len(traj), 40
+    rng = np.random.default_rng(5)
+    ids = np.stack([rng.choice(V, size=k, replace=False) for _ in range(n)]).astype(np.int32)
+    for r in range(n):
+        # rows 2m and 2m + 1 meet at pack 224 (2m + 1), inside a 1 KiB span:
+        # c = 0 puts support at both edges, 1 only the first row's, 2 only the
+        # second's, 3 neither
+        c = (r // 2) % 4
+        head, tail = c in (0, 2), c in (0, 1)  # support in the row's first / last pack
+        row = [x for x in ids[r] if 8 <= x < V - 8]
+        if head:
+            row = [1] + row
+        if tail:
+            row = [V - 2] + row
+        ids[r] = np.array((row + [x for x in range(V) if x not in row])[:k], np.int32)
+    vals = np.take_along_axis(_f32(zt_h), ids.astype(np.int64), axis=1).astype(np.float32)
+    (loss, g, gk, stats, kl, ws), ref, _ = _run(zs_h, ids, vals, traj, turn, mask, grad=grad)
+    check_loss(loss, ref.loss)
+    check_token_kl(kl, ref.kl, mask)
+    check_topk_grads(gk, g, ref, ids, 1.0, list(range(n)), mask, dtype == "bf16")
+
+
 def test_topk_in_place_forward_only_and_scale(gpu):
     traj, turn, mask, zs_h, zt_h = make_batch(71, V=8192, dtype="bf16")
     ids, vals = _support(_f32(zt_h), 50)
