@@ -6,7 +6,8 @@ import pytest
 import torch
 
 import synth
-from gpu_support import (check_grad_rows, check_loss, check_segments, check_stats,
+from gpu_support import (check_grad_every_row_on_device, check_grad_rows,
+                         check_grad_rows_batched, check_loss, check_segments, check_stats,
                          check_token_kl, device_row_source, ids_to_device, log, oracle_dtype,
                          sample_rows, to_device_logits)
 from oracle import diagnostics as D
@@ -182,13 +183,13 @@ def test_topk_floor_and_outcome_parity(gpu):
 def test_long_horizon_full_size_with_the_paper_floor(gpu):
     """65,536 tokens x V = 151,936 bf16 with App. D's floor (8, 0.15): n_min =
     8 over 30 trajectories leaves the deepest turns invalid.  Loss, per-token
-    KL, both statistics over every row; gradient on sampled rows."""
+    KL, both statistics over every row; every gradient row on the device and
+    1,000 supervised rows against the oracle, half of them at invalid turns."""
     w = synth.make("long_horizon")
     zs, zt = w.device_logits()
     succ = (w.traj_id % 2 == 0).astype(np.uint8)
-    rows = sample_rows(w.loss_mask, 24, 4, seed=3)
     ref = O.fwd_bwd(w.traj_id, w.turn_id, w.loss_mask, 0.5, w.max_turns,
-                    device_row_source(zs, zt), oracle_dtype(zs.dtype), 1.0, rows,
+                    device_row_source(zs, zt), oracle_dtype(zs.dtype), 1.0,
                     support_floor=8, support_frac=0.15, success=succ)
     log(f"  oracle done: loss={ref.loss}")
     surv = O.turn_survivors(ref.seg, w.max_turns)
@@ -200,8 +201,19 @@ def test_long_horizon_full_size_with_the_paper_floor(gpu):
     check_token_kl(kl, ref.kl, w.loss_mask)
     check_stats(stats, ref.stats)
     _check_outcome(ostats, ref.outcome_stats, w.max_turns)
-    worst = check_grad_rows(g, ref, 1.0, rows, w.loss_mask)
-    log(f"  loss gpu={loss.tolist()} ref={ref.loss} grad err={worst:.1e}")
+    check_grad_every_row_on_device(g, w.loss_mask, ref.w, 1.0)
+    # supervised rows at turns the floor invalidates (their weights keep only
+    # the trajectory term) and others, from both ends of the ticket order
+    sup = np.nonzero(w.loss_mask)[0]
+    invalid = np.isin(w.turn_id[sup], np.nonzero((surv > 0) & (surv < 8))[0])
+    rng = np.random.default_rng(3)
+    pick = lambda a, k: a if a.size <= k else rng.choice(a, k, replace=False)
+    rows = np.union1d(np.union1d(pick(sup[invalid], 500), pick(sup[~invalid], 400)),
+                      np.concatenate([sup[:50], sup[-50:]]))
+    worst = check_grad_rows_batched(g, ref.w, 1.0, rows, device_row_source(zs, zt),
+                                    oracle_dtype(zs.dtype))
+    log(f"  loss gpu={loss.tolist()} ref={ref.loss} {rows.size} oracle rows "
+        f"({int(invalid.sum())} supervised tokens at invalid turns) grad err={worst:.1e}")
     # the host diagnostics on the device statistics agree with the oracle's
     # diagnostics on the oracle's statistics
     n_b = int(np.unique(w.traj_id[(w.traj_id >= 0) & (w.loss_mask > 0)]).size)

@@ -205,10 +205,34 @@ def test_topk_bad_id_is_a_device_error(gpu):
     torch.cuda.synchronize()
 
 
+def check_topk_dense_on_device(dense, gk, ids, mask, block=4096):
+    """Every row of a dense top-K gradient, on the device: unsupervised rows
+    are zero; a supervised row is zero off its support and holds, at its
+    support ids, the sparse gradient rounded to the dense dtype."""
+    dev = dense.device
+    n = dense.shape[0]
+    mask_d = torch.from_numpy(np.asarray(mask)).to(dev).bool()
+    for r0 in range(0, n, block):
+        r1 = min(n, r0 + block)
+        d = dense[r0:r1]
+        m = mask_d[r0:r1]
+        assert torch.count_nonzero(d[~m]).item() == 0, ("unsupervised rows", r0)
+        at = ids[r0:r1].long()
+        got = torch.gather(d, 1, at)
+        want = gk[r0:r1].to(dense.dtype)
+        bits = (lambda t: t.view(torch.int16)) if dense.dtype == torch.bfloat16 else (lambda t: t)
+        assert torch.equal(bits(got[m]), bits(want[m])), ("support values", r0)
+        off = d.clone()
+        off.scatter_(1, at, torch.zeros_like(got))
+        assert torch.count_nonzero(off[m]).item() == 0, ("off-support entries", r0)
+        del off, got, want
+
+
 def test_topk_full_size_long_horizon(gpu):
     """65,536 tokens x V = 151,936 bf16, the teacher's top-50 from the
-    device-generated teacher logits; loss, KL and stats over every row, the
-    gradient on sampled rows."""
+    device-generated teacher logits, gradient in place; loss, KL and stats
+    over every row, the gradient on the support of every supervised row
+    against the oracle, and every row of the dense gradient on the device."""
     w = synth.make("long_horizon")
     zs, zt = w.device_logits()
     top_v, top_i = torch.topk(zt, 50, dim=1)  # bf16 values are exact in fp32
@@ -236,6 +260,14 @@ def test_topk_full_size_long_horizon(gpu):
     check_token_kl(kl, ref.kl, w.loss_mask)
     check_stats(stats, ref.stats)
     check_topk_grads(gk, g, ref, ids_h, 1.0, rows, w.loss_mask, True)
-    log(f"  loss gpu={loss.tolist()} ref={ref.loss}")
+    # the sparse gradient of every supervised row (unweighted, against the oracle)
+    sup = np.nonzero(w.loss_mask)[0]
+    gk_h = gk.cpu().numpy().astype(np.float64)
+    g_ref = np.stack([ref.grads[int(r)] for r in sup])
+    err = np.abs(gk_h[sup] / ref.w[sup][:, None] - g_ref)
+    assert np.all(err <= 1e-4 * np.abs(g_ref) + 2e-6), float(err.max())
+    assert np.all(gk_h[w.loss_mask == 0] == 0.0)
+    check_topk_dense_on_device(g, gk, ids, w.loss_mask)
+    log(f"  loss gpu={loss.tolist()} ref={ref.loss}; {sup.size} sparse rows, every dense row")
     del zs, g
     torch.cuda.empty_cache()
