@@ -71,17 +71,36 @@ def cpu_model() -> str | None:
     return None
 
 
-def cpu_baseline(w, sample_tokens: int):
+def host_rows_of(zs, zt, rows, batch: int = 2048):
+    """Host copies (bit patterns) of the listed rows of the device logits, the
+    CPU oracle's input: the same bits the host generator would write."""
+    import numpy as np
+    import torch
+    rows = np.asarray(rows, np.int64)
+    bits = np.uint16 if zs.dtype == torch.bfloat16 else np.float32
+    view = torch.int16 if zs.dtype == torch.bfloat16 else torch.float32
+    hs = np.empty((rows.size, zs.shape[1]), dtype=bits)
+    ht = np.empty((rows.size, zs.shape[1]), dtype=bits)
+    for k0 in range(0, rows.size, batch):
+        idx = torch.from_numpy(rows[k0:k0 + batch]).to(zs.device)
+        hs[k0:k0 + idx.numel()] = zs.index_select(0, idx).view(view).cpu().numpy().view(bits)
+        ht[k0:k0 + idx.numel()] = zt.index_select(0, idx).view(view).cpu().numpy().view(bits)
+    return hs, ht
+
+
+def cpu_baseline(w, sample_tokens: int, host_rows):
     """The float64 oracle, timed on a prefix of the batch (all its rows,
-    loss, gradient of every supervised row and per-turn stats)."""
+    loss, gradient of every supervised row and per-turn stats).  host_rows:
+    the supervised rows of that prefix, copied from the device before the
+    clock starts, with row_at[i] their position."""
     import numpy as np
     from oracle import turnkl_oracle as O
 
     n = min(sample_tokens, w.n_tokens)
     traj, turn, mask = w.traj_id[:n], w.turn_id[:n], w.loss_mask[:n]
     sup = np.nonzero(mask)[0]
-    zs, zt = w.host_rows(np.arange(n))  # generated before the clock starts
-    src = lambda rows: (zs[rows], zt[rows])
+    (hs, ht), row_at = host_rows
+    src = lambda rows: (hs[row_at[rows]], ht[row_at[rows]])
     t0 = time.perf_counter()
     ref = O.fwd_bwd(traj, turn, mask, w.alphas[0], w.max_turns, src, O.DTYPE_BF16, 1.0,
                     grad_rows=sup)
@@ -90,8 +109,8 @@ def cpu_baseline(w, sample_tokens: int):
     return {"value": n / dt, "unit": "tokens/s", "cores": O.max_threads(), "kind": "oracle",
             "cpu_model": cpu_model(), "host_cpus": os.cpu_count(),
             "sample": (f"the whole batch" if n == w.n_tokens else f"first {n} tokens of the batch")
-                      + f" ({sup.size} supervised rows, full vocabulary {w.vocab}, logits generated "
-                        f"before the clock starts), {dt:.1f} s"}
+                      + f" ({sup.size} supervised rows, full vocabulary {w.vocab}, logits copied "
+                        f"to the host before the clock starts), {dt:.1f} s"}
 
 
 def success_stand_in(w):
@@ -437,6 +456,14 @@ def main() -> int:
     # from a pristine copy, made before the call's events are recorded.
     in_place = w.in_place and not args.out_of_place
     pristine = zs.clone() if in_place else None
+    # the CPU oracle's input: the supervised rows of its sample, copied now
+    # (an in-place call overwrites the student logits)
+    cpu_rows = None
+    if not args.no_cpu_baseline:
+        sup_rows = np.nonzero(w.loss_mask[:min(args.cpu_sample_tokens, n)])[0]
+        row_at = np.full(n, -1, np.int64)
+        row_at[sup_rows] = np.arange(sup_rows.size)
+        cpu_rows = (host_rows_of(zs, zt, sup_rows), row_at)
     grad = zs if in_place else torch.empty_like(zs)
     stats = T.new_turn_stats(w.max_turns, device=dev)
     kl = torch.empty(n, dtype=torch.float32, device=dev)
@@ -552,7 +579,8 @@ def main() -> int:
     del zs, zt
     torch.cuda.empty_cache()
     if not args.no_cpu_baseline:
-        out["cpu_baseline"] = cpu_baseline(w, args.cpu_sample_tokens)
+        out["cpu_baseline"] = cpu_baseline(w, args.cpu_sample_tokens, cpu_rows)
+        del cpu_rows
         out["cpu_baseline"]["depth_controller_update_us"] = oracle_controller_timing(stats_np, w)
         if topk_host is not None:
             out["cpu_baseline"]["topk_tokens_per_s"] = oracle_topk_timing(w, topk_host)

@@ -15,7 +15,7 @@ class SynthParams(ctypes.Structure):
         ("ld", ctypes.c_int64),
         ("dtype", ctypes.c_int32),
         ("n_peaks", ctypes.c_int32),
-        ("student_scale", ctypes.c_float),
+        ("student_sigma", ctypes.c_float),
         ("peak_boost", ctypes.c_float),
         ("shift_threshold", ctypes.c_uint32),
         ("reserved", ctypes.c_uint32),
@@ -47,12 +47,12 @@ def lib():
     return _lib
 
 
-def fill_host(params: SynthParams, teacher_scale: np.ndarray, r0: int, r1: int,
+def fill_host(params: SynthParams, teacher_sigma: np.ndarray, r0: int, r1: int,
               zs: np.ndarray | None, zt: np.ndarray | None, n_threads: int = 0) -> None:
     """Write rows [r0, r1) into host arrays whose first row is row r0."""
     if n_threads <= 0:
         n_threads = min(16, os.cpu_count() or 1)
-    ts = np.ascontiguousarray(teacher_scale, dtype=np.float32)
+    ts = np.ascontiguousarray(teacher_sigma, dtype=np.float32)
     rc = lib().synth_fill_host(ctypes.byref(params), ts.ctypes.data, r0, r1,
                                None if zs is None else zs.ctypes.data,
                                None if zt is None else zt.ctypes.data, n_threads)
@@ -60,12 +60,12 @@ def fill_host(params: SynthParams, teacher_scale: np.ndarray, r0: int, r1: int,
         raise RuntimeError(f"synth_fill_host failed ({rc})")
 
 
-def fill_host_rows(params: SynthParams, teacher_scale: np.ndarray, rows: np.ndarray,
+def fill_host_rows(params: SynthParams, teacher_sigma: np.ndarray, rows: np.ndarray,
                    zs: np.ndarray | None, zt: np.ndarray | None, n_threads: int = 0) -> None:
     """Write the listed rows (absolute indices) into consecutive rows of host arrays."""
     if n_threads <= 0:
         n_threads = min(16, os.cpu_count() or 1)
-    ts = np.ascontiguousarray(teacher_scale, dtype=np.float32)
+    ts = np.ascontiguousarray(teacher_sigma, dtype=np.float32)
     r = np.ascontiguousarray(rows, dtype=np.int64)
     rc = lib().synth_fill_host_rows(ctypes.byref(params), ts.ctypes.data, r.ctypes.data, r.shape[0],
                                     None if zs is None else zs.ctypes.data,
@@ -74,10 +74,10 @@ def fill_host_rows(params: SynthParams, teacher_scale: np.ndarray, rows: np.ndar
         raise RuntimeError(f"synth_fill_host_rows failed ({rc})")
 
 
-def fill_device(params: SynthParams, teacher_scale_ptr: int, r0: int, r1: int,
+def fill_device(params: SynthParams, teacher_sigma_ptr: int, r0: int, r1: int,
                 zs_ptr: int | None, zt_ptr: int | None, stream: int) -> None:
     """Write rows [r0, r1) into device buffers whose first row is row r0."""
-    rc = lib().synth_fill_device(ctypes.byref(params), teacher_scale_ptr, r0, r1,
+    rc = lib().synth_fill_device(ctypes.byref(params), teacher_sigma_ptr, r0, r1,
                                  zs_ptr, zt_ptr, stream)
     if rc != 0:
         raise RuntimeError(f"synth_fill_device failed ({rc})")

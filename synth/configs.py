@@ -26,7 +26,6 @@ import numpy as np
 from . import _lib
 
 SEED_BASE = 20260700
-SQRT3_OVER_65536 = math.sqrt(3.0) / 65536.0
 
 BF16 = "bf16"
 F32 = "f32"
@@ -41,7 +40,7 @@ class Workload:
     traj_id: np.ndarray        # int32 [N], sorted, -1 = padding
     turn_id: np.ndarray        # int32 [N]
     loss_mask: np.ndarray      # uint8 [N], 1 = supervised response token
-    teacher_scale: np.ndarray  # float32 [N], teacher-noise sigma * sqrt(3)/65536
+    teacher_sigma: np.ndarray  # float32 [N], standard deviation of the teacher noise per row
     seed: int
     student_sigma: float
     n_peaks: int = 0
@@ -70,7 +69,7 @@ class Workload:
         p.ld = self.vocab if ld is None else ld
         p.dtype = 0 if self.dtype == BF16 else 1
         p.n_peaks = self.n_peaks
-        p.student_scale = float(np.float32(self.student_sigma * SQRT3_OVER_65536))
+        p.student_sigma = float(np.float32(self.student_sigma))
         p.peak_boost = float(np.float32(self.peak_boost))
         p.shift_threshold = int(round(self.shift_prob * 2.0 ** 32)) if self.shift_prob > 0 else 0
         p.reserved = 0
@@ -81,7 +80,7 @@ class Workload:
         dt = np.uint16 if self.dtype == BF16 else np.float32
         zs = np.empty((r1 - r0, self.vocab), dtype=dt)
         zt = np.empty((r1 - r0, self.vocab), dtype=dt)
-        _lib.fill_host(self.params(), self.teacher_scale, r0, r1, zs, zt, n_threads)
+        _lib.fill_host(self.params(), self.teacher_sigma, r0, r1, zs, zt, n_threads)
         return zs, zt
 
     def host_rows(self, rows, n_threads: int = 0):
@@ -90,7 +89,7 @@ class Workload:
         dt = np.uint16 if self.dtype == BF16 else np.float32
         zs = np.empty((rows.shape[0], self.vocab), dtype=dt)
         zt = np.empty((rows.shape[0], self.vocab), dtype=dt)
-        _lib.fill_host_rows(self.params(), self.teacher_scale, rows, zs, zt, n_threads)
+        _lib.fill_host_rows(self.params(), self.teacher_sigma, rows, zs, zt, n_threads)
         return zs, zt
 
     def device_logits(self, ld: int | None = None, device: str = "cuda"):
@@ -105,7 +104,7 @@ class Workload:
         n = self.n_tokens
         zs = torch.empty((n, ld), dtype=tdt, device=device)
         zt = torch.empty((n, ld), dtype=tdt, device=device)
-        ts = torch.from_numpy(self.teacher_scale).to(device)
+        ts = torch.from_numpy(self.teacher_sigma).to(device)
         stream = torch.cuda.current_stream().cuda_stream
         if n:
             _lib.fill_device(self.params(ld), ts.data_ptr(), 0, n, zs.data_ptr(), zt.data_ptr(),
@@ -137,8 +136,8 @@ def _pack(turn_lengths: list[list[int]], obs_fracs: list[float]):
     return (np.concatenate(traj), np.concatenate(turn), np.concatenate(mask))
 
 
-def _scale(sigma) -> np.ndarray:
-    return np.asarray(np.asarray(sigma, np.float64) * SQRT3_OVER_65536, dtype=np.float32)
+def _sigma(sigma) -> np.ndarray:
+    return np.asarray(sigma, dtype=np.float32)
 
 
 def _largest_remainder(lengths: np.ndarray, total: int, minimum: int) -> np.ndarray:
@@ -176,7 +175,7 @@ def tiny() -> Workload:
     return Workload(
         name="tiny", description="2 trajectories x 4 turns, turn lengths U{8..32}, V=1024 fp32",
         vocab=1024, dtype=F32, traj_id=traj, turn_id=turn, loss_mask=mask,
-        teacher_scale=np.full(traj.shape, _scale(0.5), np.float32), seed=seed,
+        teacher_sigma=np.full(traj.shape, _sigma(0.5), np.float32), seed=seed,
         student_sigma=2.0, alphas=(0.5,), max_turns=4)
 
 
@@ -188,7 +187,7 @@ def agent() -> Workload:
     return Workload(
         name="agent", description="8 trajectories x 10 turns, turn lengths U{16..96}, 40% observation"
         "-masked, V=32000 bf16", vocab=32000, dtype=BF16, traj_id=traj, turn_id=turn,
-        loss_mask=mask, teacher_scale=np.full(traj.shape, _scale(1.0), np.float32), seed=seed,
+        loss_mask=mask, teacher_sigma=np.full(traj.shape, _sigma(1.0), np.float32), seed=seed,
         student_sigma=3.0, alphas=(0.25,), max_turns=10)
 
 
@@ -201,7 +200,7 @@ def peaked() -> Workload:
         name="peaked", description="16 trajectories x 30 turns, turn lengths U{8..60}, 60% observation"
         "-masked, 5 peaked columns per row (+10, teacher peaks re-drawn on 20% of rows), "
         "V=151936 bf16", vocab=151936, dtype=BF16, traj_id=traj, turn_id=turn, loss_mask=mask,
-        teacher_scale=np.full(traj.shape, _scale(1.0), np.float32), seed=seed, student_sigma=3.0,
+        teacher_sigma=np.full(traj.shape, _sigma(1.0), np.float32), seed=seed, student_sigma=3.0,
         n_peaks=5, peak_boost=10.0, shift_prob=0.2, alphas=(0.0, 0.25, 0.5, 1.0), max_turns=30)
 
 
@@ -224,7 +223,7 @@ def long_horizon(n_tokens: int = 65536) -> Workload:
         name="long_horizon", description=f"{len(lens)} trajectories, turns U{{20..50}}, turn lengths "
         f"lognormal(4, 0.6) clipped to [4, 512], cut at {n_tokens} tokens, 40% observation-masked, "
         "teacher noise 1.5*0.95^turn, V=151936 bf16", vocab=151936, dtype=BF16, traj_id=traj,
-        turn_id=turn, loss_mask=mask, teacher_scale=_scale(sigma_t), seed=seed, student_sigma=3.0,
+        turn_id=turn, loss_mask=mask, teacher_sigma=_sigma(sigma_t), seed=seed, student_sigma=3.0,
         alphas=(0.5,), max_turns=50)
 
 
@@ -258,7 +257,7 @@ def stress(n_tokens: int = 131072) -> Workload:
         "{1..200}, lognormal turn lengths rescaled to the total, mixed masks (one fully masked turn, "
         "one fully masked trajectory), V=151936 bf16, gradient written in place", vocab=151936,
         dtype=BF16, traj_id=traj, turn_id=turn, loss_mask=mask,
-        teacher_scale=np.full(traj.shape, _scale(1.0), np.float32), seed=seed, student_sigma=3.0,
+        teacher_sigma=np.full(traj.shape, _sigma(1.0), np.float32), seed=seed, student_sigma=3.0,
         alphas=(0.75,), max_turns=200, in_place=True)
 
 

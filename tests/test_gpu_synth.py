@@ -22,7 +22,7 @@ def test_device_generator_matches_host_bits(name, gpu):
     dt = torch.bfloat16 if w.dtype == synth.configs.BF16 else torch.float32
     zs = torch.empty((len(rows), ld), dtype=dt, device=gpu)
     zt = torch.empty((len(rows), ld), dtype=dt, device=gpu)
-    ts = torch.from_numpy(w.teacher_scale).to(gpu)
+    ts = torch.from_numpy(w.teacher_sigma).to(gpu)
     stream = torch.cuda.current_stream().cuda_stream
     es = 2 if dt == torch.bfloat16 else 4
     for k, r in enumerate(rows.tolist()):
