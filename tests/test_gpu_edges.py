@@ -387,6 +387,38 @@ def test_single_giant_segment_and_one_token_segments(gpu):
     check_all(out, ref, mask, 1.0, rows)
 
 
+def test_batch_beyond_the_fused_scan(gpu):
+    """2,200,000 tokens: more than 2,048 tiles of 1,024 tokens, so the segment
+    kernels take the separate scan of the tile counts instead of summing them
+    in every workgroup.  Several thousand trajectories with padding between
+    some turns, V = 16."""
+    rng = np.random.default_rng(47)
+    n_target, V = 2_200_000, 16
+    lens = rng.integers(1, 120, size=n_target // 30)
+    lens = lens[:np.searchsorted(np.cumsum(lens), n_target) + 1]
+    turns_per_traj = rng.integers(1, 40, size=lens.size)
+    traj_of_seg = np.repeat(np.arange(turns_per_traj.size), turns_per_traj)[:lens.size]
+    turn_of_seg = np.concatenate([np.sort(rng.choice(60, size=k, replace=False))
+                                  for k in turns_per_traj])[:lens.size]
+    traj = np.repeat(traj_of_seg, lens).astype(np.int32)
+    turn = np.repeat(turn_of_seg, lens).astype(np.int32)
+    mask = (rng.uniform(size=traj.size) < 0.6).astype(np.uint8)
+    # padding runs replace the first tokens of every 50th segment
+    starts = np.concatenate([[0], np.cumsum(lens)[:-1]])
+    for s0, ln in zip(starts[::50], lens[::50]):
+        k = min(3, int(ln) - 1)
+        traj[s0:s0 + k], turn[s0:s0 + k], mask[s0:s0 + k] = -1, 0, 0
+    n = traj.size
+    assert n > 2048 * 1024
+    zs = bf16_bits(rng.normal(0, 3, (n, V)))
+    zt = bf16_bits(rng.normal(0, 3, (n, V)))
+    log(f"fallback scan: N={n} segments={lens.size}")
+    out, ref, rows = run_both(traj, turn, mask, zs, zt, max_turns=60,
+                              grad_rows=list(range(0, n, 4099)))
+    assert ref.status == O.OK
+    check_all(out, ref, mask, 1.0, rows)
+
+
 def test_extreme_but_finite_logits(gpu):
     traj, turn, mask, zs, zt = make_batch(43, V=2048, dtype="f32", sigma=20.0, noise=5.0)
     zs[::3] -= 1e4
