@@ -122,6 +122,46 @@ def test_topk_support_at_row_ends(dtype, V, grad, gpu):
     check_topk_grads(gk, g, ref, ids, 1.0, list(range(n)), mask, dtype == "bf16")
 
 
+@pytest.mark.parametrize("dtype,V,ld,k", [
+    ("bf16", 4116, 4128, 50),  # padded row stride; ids in the partial last 64-byte span
+    ("f32", 2056, 2064, 50),   # the same for fp32 (16 elements per span)
+    ("bf16", 4096, 4096, 64),  # 64 ids packed into two spans: every slot taken
+    ("bf16", 4096, 4100, 50),  # rows not 64-byte aligned
+])
+def test_topk_clustered_support(dtype, V, ld, k, gpu):
+    """Out-of-place dense gradient with the support ids packed into a few
+    64-byte spans per row (neighbouring support values share cache lines and
+    sectors), some of them in the row's partial last span, under a padded
+    row stride.  Every element of every row is compared, and the padding
+    columns of the gradient are never written."""
+    log(f"topk clustered support {dtype} V={V} ld={ld} K={k}")
+    traj, turn, mask, zs_h, zt_h = make_batch(131, V=V, dtype=dtype)
+    n = len(traj)
+    per = 32 if dtype == "bf16" else 16
+    n_sec = -(-V // per)
+    rng = np.random.default_rng(9)
+    ids = np.empty((n, k), np.int32)
+    for r in range(n):
+        want = -(-k // per) + (r % 3)  # as few sectors as hold k ids, or one or two more
+        secs = rng.choice(n_sec - 1, size=want, replace=False)
+        if r % 2 == 0:
+            secs[0] = n_sec - 1  # the last (possibly partial) sector
+        cols = np.concatenate([np.arange(s * per, min((s + 1) * per, V)) for s in secs])
+        if cols.size < k:
+            cols = np.concatenate([cols, np.setdiff1d(np.arange(V), cols)[:k - cols.size]])
+        ids[r] = rng.permutation(rng.choice(cols, size=k, replace=False))
+    vals = np.take_along_axis(_f32(zt_h), ids.astype(np.int64), axis=1).astype(np.float32)
+    tdt = torch.bfloat16 if dtype == "bf16" else torch.float32
+    buf = torch.full((n, ld), float("nan"), dtype=tdt, device=gpu)
+    (loss, g, gk, stats, kl, ws), ref, _ = _run(zs_h, ids, vals, traj, turn, mask,
+                                                grad=buf[:, :V])
+    check_loss(loss, ref.loss)
+    check_token_kl(kl, ref.kl, mask)
+    check_topk_grads(gk, g, ref, ids, 1.0, list(range(n)), mask, dtype == "bf16")
+    if ld > V:
+        assert torch.isnan(buf[:, V:].float()).all().item()
+
+
 def test_topk_in_place_forward_only_and_scale(gpu):
     traj, turn, mask, zs_h, zt_h = make_batch(71, V=8192, dtype="bf16")
     ids, vals = _support(_f32(zt_h), 50)
