@@ -113,7 +113,6 @@ __global__ __launch_bounds__(kSegThreads) void seg_count(SegParams p, Ws ws, int
     ws.blk_cnt[blockIdx.x] = c;
     ws.blk_err[blockIdx.x] = e;
   }
-  drain_stores();
 }
 
 constexpr int kScanThreads = 1024;

@@ -387,6 +387,23 @@ def test_single_giant_segment_and_one_token_segments(gpu):
     check_all(out, ref, mask, 1.0, rows)
 
 
+def test_trajectory_with_thousands_of_turns(gpu):
+    """One trajectory of 2,600 one-token turns, then one of 400: the segments
+    of the first lie up to 2,599 segments after their trajectory's first, so
+    the search for each segment's head leaves the 2,048 segment ids a
+    workgroup holds in LDS."""
+    rng = np.random.default_rng(48)
+    V, n1, n2 = 64, 2600, 400
+    traj = np.concatenate([np.zeros(n1, np.int32), np.ones(n2, np.int32)])
+    turn = np.concatenate([np.arange(n1), np.arange(n2)]).astype(np.int32)
+    mask = (rng.uniform(size=n1 + n2) < 0.7).astype(np.uint8)
+    zs = bf16_bits(rng.normal(0, 3, (n1 + n2, V)))
+    zt = bf16_bits(rng.normal(0, 3, (n1 + n2, V)))
+    out, ref, rows = run_both(traj, turn, mask, zs, zt, max_turns=n1,
+                              grad_rows=list(range(0, n1 + n2, 37)))
+    check_all(out, ref, mask, 1.0, rows)
+
+
 def test_batch_beyond_the_fused_scan(gpu):
     """2,200,000 tokens: more than 2,048 tiles of 1,024 tokens, so the segment
     kernels take the separate scan of the tile counts instead of summing them
