@@ -282,6 +282,52 @@ def test_runs_are_bitwise_deterministic(gpu):
         assert torch.equal(st, outs[0][2])
 
 
+@pytest.mark.parametrize("V,vpt,all_supervised", [(37984, 2, False), (37984, 2, True),
+                                                   (151936, 0, False), (151936, 0, True)])
+def test_exchange_stress_loop(V, vpt, all_supervised, gpu):
+    """250 calls in a row (1,000 over the four cases) of a batch whose rows are
+    split over several workgroups (10 chunks per row at V = 37,984 with 2 packs
+    per thread, 3 at full width), each compared bit for bit with the first
+    call on the device: loss, per-token KL, statistics and gradient.  A mixed
+    batch runs the split load order, an all-supervised one the alternating
+    order.  The first call is checked against the oracle."""
+    traj, turn, mask, zs_h, zt_h = make_batch(15 + V % 7, V=V, n_traj=5, max_len=30)
+    if all_supervised:
+        mask = (traj >= 0).astype(np.uint8)
+    zs, zt = to_device_logits(zs_h), to_device_logits(zt_h)
+    turn_d, traj_d, mask_d = ids_to_device(traj, turn, mask)
+    n = len(traj)
+    log(f"exchange stress: N={n} V={V} vpt={vpt} all_supervised={all_supervised}")
+    T.set_row_tiling(vpt)
+    try:
+        ws = T.Workspace(n, V, T.BF16, 8)
+        grad = torch.empty_like(zs)
+        kl = torch.empty(n, dtype=torch.float32, device=gpu)
+        st = T.new_turn_stats(8)
+        loss, *_ = T.fwd_bwd(zs, zt, turn_d, traj_d, mask_d, 0.6, grad=grad, max_turns=8,
+                             turn_stats=st, token_kl=kl, workspace=ws)
+        ref = (loss.clone(), grad.clone(), kl.clone(), st.clone())
+        bad = torch.zeros(4, dtype=torch.int64, device=gpu)
+        for _ in range(250):
+            loss, *_ = T.fwd_bwd(zs, zt, turn_d, traj_d, mask_d, 0.6, grad=grad, max_turns=8,
+                                 turn_stats=st, token_kl=kl, workspace=ws, check=False)
+            bad[0] += (loss != ref[0]).sum()
+            bad[1] += (grad.view(torch.int16) != ref[1].view(torch.int16)).sum()
+            bad[2] += (kl.view(torch.int32) != ref[2].view(torch.int32)).sum()
+            bad[3] += (st != ref[3]).sum()
+        torch.cuda.synchronize()
+        assert ws.status() == T.OK
+    finally:
+        T.set_row_tiling(0)
+    assert bad.tolist() == [0, 0, 0, 0]
+    o = O.fwd_bwd(traj, turn, mask, 0.6, 8, lambda r: (zs_h[r], zt_h[r]), O.DTYPE_BF16, 1.0,
+                  list(range(0, n, 7)))
+    check_loss(ref[0], o.loss)
+    check_token_kl(ref[2], o.kl, mask)
+    check_stats(ref[3], o.stats)
+    check_grad_rows(ref[1], o, 1.0, list(range(0, n, 7)), mask)
+
+
 def test_accumulated_stats_equal_pooled_oracle(gpu):
     """Three micro-batches accumulated on the device equal the oracle's
     statistics recomputed from the pooled tokens (no merge formula)."""
