@@ -63,7 +63,7 @@ def frame(traj, turn, mask, kl, w=None):
     return pd.DataFrame(d)
 
 
-_settings = settings(max_examples=150, deadline=None,
+_settings = settings(max_examples=150, deadline=None, derandomize=True,
                      suppress_health_check=[HealthCheck.too_slow])
 
 
